@@ -1,0 +1,204 @@
+"""CPU oracle for the KVMem per-decode-step path -- TEST INFRASTRUCTURE ONLY.
+
+A plain fp64 C implementation (kvmem_oracle.c) of what the GPU path computes,
+written from the paper (KVMem, arXiv 2609.04852), with this thin ctypes layer
+that only marshals numpy arrays.  Only the tests, the smoke check and the
+benchmark's CPU-baseline leg may import it; the HIP library never does, and
+this package never imports the HIP library.
+
+Entry points and the passages they follow:
+  mean_k            Eq. 9  (Sec. 4.3, Mean-K retrieval-index construction)
+  k_eff             Eq. 5, Eq. 7 (Sec. 3.1, active budget and view capacity)
+  block_relevance   Eq. 10 (Sec. 4.3, query-conditioned block scoring)
+  select            Sec. 4.3 selector (sink + recent reserved, top-k, chronological)
+  view_attention    Sec. 4.4 / Sec. 5.3: attention through the view's page table
+  masked_dense_attention   the same attention as dense attention with the
+                    non-view blocks masked out
+"""
+import ctypes
+import os
+
+import numpy as np
+
+MEAN_ALL = 0
+MAX_GROUP = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libkvmem_oracle.so")
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from .build import build_oracle
+        build_oracle()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64, dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    ci = ctypes.c_int
+    lib.oracle_mean_k.argtypes = [ci, ci, ci, ci, P, i64, P, i32, i32, P]
+    lib.oracle_mean_k.restype = ci
+    lib.oracle_k_eff.argtypes = [i64, i64, ci, i32, i32, i32]
+    lib.oracle_k_eff.restype = i64
+    lib.oracle_block_relevance.argtypes = [ci, ci, ci, ci, ci, P, P, i32, i32, i32, ci, dbl, P]
+    lib.oracle_block_relevance.restype = ci
+    lib.oracle_select.argtypes = [ci, P, i32, i32, i32, i64, P, P, P]
+    lib.oracle_select.restype = ci
+    lib.oracle_view_attention.argtypes = [ci, ci, ci, ci, ci, ci, P, P, P, i64, P, ci, i32, i32,
+                                          dbl, P, P]
+    lib.oracle_view_attention.restype = ci
+    lib.oracle_masked_dense_attention.argtypes = [ci, ci, ci, ci, ci, ci, P, P, P, i64, P, i32, P,
+                                                  ci, i32, i32, dbl, P, P]
+    lib.oracle_masked_dense_attention.restype = ci
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ci
+    _lib = lib
+    return lib
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a)
+    if a.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {a.dtype}")
+    return a
+
+
+def _pool(pool):
+    """A K/V pool is float32 or bf16 stored as raw uint16 bits."""
+    pool = np.ascontiguousarray(pool)
+    if pool.dtype == np.float32:
+        return pool, 0
+    if pool.dtype == np.uint16:
+        return pool, 1
+    raise TypeError("pool must be float32 or uint16 (bf16 bits)")
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what}: invalid arguments")
+
+
+def num_threads() -> int:
+    return _load().oracle_num_threads()
+
+
+def mean_k(k_pool, block_to_page, first_block=0, n_blocks=None, index=None):
+    """Eq. 9.  k_pool [P][Hkv][Bt][d]; returns/updates index [M][Hkv][d] float32."""
+    k_pool, is_bf16 = _pool(k_pool)
+    n_pages, hkv, bt, d = k_pool.shape
+    b2p = _c(block_to_page, np.int32)
+    m = b2p.shape[0]
+    if n_blocks is None:
+        n_blocks = m - first_block
+    if index is None:
+        index = np.zeros((m, hkv, d), np.float32)
+    if index.dtype != np.float32 or not index.flags.c_contiguous or index.shape != (m, hkv, d):
+        raise TypeError("index must be a C-contiguous float32 [M][Hkv][d] array")
+    if first_block < 0 or n_blocks < 0 or first_block + n_blocks > m:
+        raise ValueError("block range out of bounds")
+    rc = _load().oracle_mean_k(hkv, bt, d, is_bf16, k_pool.ctypes.data, n_pages,
+                               b2p.ctypes.data, first_block, n_blocks, index.ctypes.data)
+    _check(rc, "mean_k")
+    return index
+
+
+def k_eff(model_ctx_tokens, gpu_kv_tokens, block_tokens, n_blocks, n_sink, n_recent):
+    """Eq. 5 / Eq. 7.  Returns k_eff, or raises when the budget cannot hold the mandatory context."""
+    k = _load().oracle_k_eff(int(model_ctx_tokens), int(gpu_kv_tokens), int(block_tokens),
+                             int(n_blocks), int(n_sink), int(n_recent))
+    if k < 0:
+        raise ValueError("budget below the mandatory sink+recent context, or bad shape")
+    return int(k)
+
+
+def block_relevance(q, index, n_sink, n_recent, mode=MEAN_ALL, scale=0.0):
+    """Eq. 10.  q [L][n_q][Hq][d] float32, index [L][M][Hkv][d] float32.
+
+    Returns R float64 [n_sel][M] (n_sel = 1 for MEAN_ALL, L*Hkv for MAX_GROUP);
+    reserved blocks hold +inf."""
+    q = _c(q, np.float32)
+    index = _c(index, np.float32)
+    if q.ndim != 4 or index.ndim != 4 or q.shape[0] != index.shape[0] or q.shape[3] != index.shape[3]:
+        raise ValueError("q must be [L][n_q][Hq][d] and index [L][M][Hkv][d]")
+    L, nq, hq, d = q.shape
+    _, m, hkv, _ = index.shape
+    n_sel = 1 if mode == MEAN_ALL else L * hkv
+    out = np.empty((n_sel, m), np.float64)
+    rc = _load().oracle_block_relevance(L, nq, hq, hkv, d, q.ctypes.data, index.ctypes.data, m,
+                                        n_sink, n_recent, mode, float(scale), out.ctypes.data)
+    _check(rc, "block_relevance")
+    return out
+
+
+def select(relevance, n_sink, n_recent, k, block_to_page):
+    """Selector.  relevance [n_sel][M] float64 -> (view_blocks, view_pages) int32 [n_sel][n_view]."""
+    r = _c(relevance, np.float64)
+    if r.ndim == 1:
+        r = r[None, :]
+    n_sel, m = r.shape
+    b2p = _c(block_to_page, np.int32)
+    if b2p.shape[0] != m:
+        raise ValueError("block_to_page length must equal the number of blocks")
+    n_view = n_sink + k + n_recent
+    vb = np.empty((n_sel, n_view), np.int32)
+    vp = np.empty((n_sel, n_view), np.int32)
+    rc = _load().oracle_select(n_sel, r.ctypes.data, m, n_sink, n_recent, int(k), b2p.ctypes.data,
+                               vb.ctypes.data, vp.ctypes.data)
+    _check(rc, "select")
+    return vb, vp
+
+
+def view_attention(q, k_pool, v_pool, view_pages, last_page_tokens=None, scale=0.0):
+    """Attention through the page table.  q [n_q][Hq][d] float32 (one layer);
+    pools [P][Hkv][Bt][d]; view_pages [n_sel][n_view].  Returns (out, lse) float64."""
+    q = _c(q, np.float32)
+    k_pool, kb = _pool(k_pool)
+    v_pool, vb = _pool(v_pool)
+    if kb != vb or k_pool.shape != v_pool.shape:
+        raise ValueError("K and V pools must match in shape and dtype")
+    n_pages, hkv, bt, d = k_pool.shape
+    vp = _c(view_pages, np.int32)
+    if vp.ndim == 1:
+        vp = vp[None, :]
+    n_sel, n_view = vp.shape
+    nq, hq, dq = q.shape
+    if dq != d:
+        raise ValueError("head_dim mismatch")
+    lpt = bt if last_page_tokens is None else int(last_page_tokens)
+    out = np.empty((nq, hq, d), np.float64)
+    lse = np.empty((nq, hq), np.float64)
+    rc = _load().oracle_view_attention(nq, hq, hkv, d, bt, kb, q.ctypes.data, k_pool.ctypes.data,
+                                       v_pool.ctypes.data, n_pages, vp.ctypes.data, n_sel, n_view,
+                                       lpt, float(scale), out.ctypes.data, lse.ctypes.data)
+    _check(rc, "view_attention")
+    return out, lse
+
+
+def masked_dense_attention(q, k_pool, v_pool, block_to_page, view_blocks, last_page_tokens=None,
+                           scale=0.0):
+    """Dense attention over all M blocks with non-view blocks masked.  Returns (out, lse) float64."""
+    q = _c(q, np.float32)
+    k_pool, kb = _pool(k_pool)
+    v_pool, vb = _pool(v_pool)
+    if kb != vb or k_pool.shape != v_pool.shape:
+        raise ValueError("K and V pools must match in shape and dtype")
+    n_pages, hkv, bt, d = k_pool.shape
+    b2p = _c(block_to_page, np.int32)
+    vbl = _c(view_blocks, np.int32)
+    if vbl.ndim == 1:
+        vbl = vbl[None, :]
+    n_sel, n_view = vbl.shape
+    nq, hq, _ = q.shape
+    lpt = bt if last_page_tokens is None else int(last_page_tokens)
+    out = np.empty((nq, hq, d), np.float64)
+    lse = np.empty((nq, hq), np.float64)
+    rc = _load().oracle_masked_dense_attention(nq, hq, hkv, d, bt, kb, q.ctypes.data,
+                                               k_pool.ctypes.data, v_pool.ctypes.data, n_pages,
+                                               b2p.ctypes.data, b2p.shape[0], vbl.ctypes.data,
+                                               n_sel, n_view, lpt, float(scale), out.ctypes.data,
+                                               lse.ctypes.data)
+    _check(rc, "masked_dense_attention")
+    return out, lse

@@ -1,0 +1,411 @@
+"""Pins for the CPU oracle: every check here comes from something other than the
+oracle itself -- a closed form, an exact rational computation, brute force over
+all subsets, a stated configuration number, or an independent library routine
+(torch's scaled_dot_product_attention in float64).  Each group names the
+passage of the paper it pins.
+"""
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_04852_amd import workload as W
+
+
+def round_to_f32(fr: Fraction) -> np.float32:
+    """Correctly rounded (nearest, ties to even) fp32 value of an exact rational."""
+    f = np.float32(float(fr))
+    cands = [np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))]
+    return min(cands, key=lambda c: (abs(Fraction(float(c)) - fr),
+                                     int(np.array(c, np.float32).view(np.uint32)) & 1))
+
+
+def rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# ---------------------------------------------------------------- Eq. 9 ---
+class TestMeanK:
+    def test_single_token_block_is_identity(self):
+        k = rng(1).standard_normal((5, 2, 1, 8)).astype(np.float32)
+        b2p = np.array([3, 0, 4, 1, 2], np.int32)
+        idx = oracle.mean_k(k, b2p)
+        np.testing.assert_array_equal(idx, k[b2p, :, 0, :])
+
+    def test_constant_block(self):
+        vals = rng(2).standard_normal((4, 3)).astype(np.float32)
+        k = np.broadcast_to(vals[:, :, None, None], (4, 3, 16, 8)).copy()
+        idx = oracle.mean_k(k, np.arange(4, dtype=np.int32))
+        np.testing.assert_array_equal(idx, np.broadcast_to(vals[:, :, None], (4, 3, 8)))
+
+    @pytest.mark.parametrize("bt", [3, 5, 16])
+    def test_exact_rational_mean_fp32(self, bt):
+        k = (rng(bt).standard_normal((3, 2, bt, 4)) * 10.0 ** rng(bt + 1).integers(-3, 3, (3, 2, bt, 4))
+             ).astype(np.float32)
+        b2p = np.array([2, 0, 1], np.int32)
+        idx = oracle.mean_k(k, b2p)
+        for b in range(3):
+            for g in range(2):
+                for j in range(4):
+                    exact = sum(Fraction(float(x)) for x in k[b2p[b], g, :, j]) / bt
+                    assert idx[b, g, j] == round_to_f32(exact)
+
+    def test_exact_rational_mean_bf16(self):
+        x = rng(7).standard_normal((3, 2, 16, 8)).astype(np.float32)
+        bits = W.bf16_bits(x)
+        vals = W.bf16_to_f32(bits)
+        b2p = np.array([1, 2, 0], np.int32)
+        idx = oracle.mean_k(bits, b2p)
+        for b in range(3):
+            for g in range(2):
+                for j in range(8):
+                    exact = sum(Fraction(float(v)) for v in vals[b2p[b], g, :, j]) / 16
+                    assert idx[b, g, j] == round_to_f32(exact)
+
+    def test_block_reads_its_page(self):
+        # page p holds the constant 100*p + g in head g
+        p, hkv = 6, 2
+        k = np.zeros((p, hkv, 4, 4), np.float32)
+        for pg in range(p):
+            for g in range(hkv):
+                k[pg, g] = 100 * pg + g
+        b2p = np.array([5, 3, 1, 0, 2, 4], np.int32)
+        idx = oracle.mean_k(k, b2p)
+        for b in range(p):
+            for g in range(hkv):
+                assert np.all(idx[b, g] == 100 * b2p[b] + g)
+
+    def test_block_range_only(self):
+        k = rng(3).standard_normal((8, 1, 4, 4)).astype(np.float32)
+        b2p = np.arange(8, dtype=np.int32)
+        idx = np.full((8, 1, 4), -7.0, np.float32)
+        oracle.mean_k(k, b2p, first_block=2, n_blocks=3, index=idx)
+        assert np.all(idx[:2] == -7.0) and np.all(idx[5:] == -7.0)
+        np.testing.assert_array_equal(idx[2:5], oracle.mean_k(k, b2p)[2:5])
+
+
+# ------------------------------------------------------- Eq. 5 / Eq. 7 ---
+class TestBudget:
+    @pytest.mark.parametrize("name", list(W.CONFIGS))
+    def test_stated_configs(self, name):
+        c = W.CONFIGS[name]
+        k = oracle.k_eff(c.budget_tokens, c.budget_tokens, c.block_tokens, c.n_blocks,
+                         c.sink_blocks, c.n_recent)
+        assert k == c.top_k
+
+    def test_active_budget_is_the_minimum(self):
+        # B_a = min(B_model, B_gpu): the smaller limit decides
+        assert oracle.k_eff(262144, 100_000, 16, 65536, 0, 512) == (100_000 - 8192) // 16
+        assert oracle.k_eff(50_000, 262144, 16, 65536, 2, 512) == (50_000 - 514 * 16) // 16
+
+    def test_capped_by_candidates(self):
+        assert oracle.k_eff(10**9, 10**9, 16, 100, 1, 4) == 95
+
+    def test_budget_below_mandatory(self):
+        with pytest.raises(ValueError):
+            oracle.k_eff(63, 10**6, 16, 100, 0, 4)
+        assert oracle.k_eff(64, 10**6, 16, 100, 0, 4) == 0
+
+
+# --------------------------------------------------------------- Eq. 10 ---
+def sigmoid(x):
+    return 1.0 / (1.0 + math.exp(-x))
+
+
+def idx4(rows):
+    """index [L=1][M][Hkv][d=4] from a nested list rows[b][g] = first coordinate."""
+    arr = np.zeros((1, len(rows), len(rows[0]), 4), np.float32)
+    for b, r in enumerate(rows):
+        for g, v in enumerate(r):
+            arr[0, b, g, 0] = v
+    return arr
+
+
+class TestRelevance:
+    def test_two_candidates_logistic(self):
+        q = np.zeros((1, 1, 1, 4), np.float32)
+        q[..., 0] = 2.0
+        index = idx4([[1.0], [0.5]])
+        r = oracle.block_relevance(q, index, 0, 0)
+        # logits 2*1/sqrt(4) = 1.0 and 0.5
+        assert r[0, 0] == pytest.approx(sigmoid(0.5), abs=1e-15)
+        assert r[0, 1] == pytest.approx(sigmoid(-0.5), abs=1e-15)
+
+    def test_gqa_grouping_and_head_mean(self):
+        # Hkv=2, Hq=4: heads 0,1 read KV head 0, heads 2,3 read KV head 1
+        a = [1.0, 3.0, -2.0, 5.0]
+        q = np.zeros((1, 1, 4, 4), np.float32)
+        q[0, 0, :, 0] = a
+        index = idx4([[0.75, 0.4], [0.25, 0.4]])  # KV head 1 cannot tell the blocks apart
+        r = oracle.block_relevance(q, index, 0, 0)
+        expect0 = (sigmoid(a[0] * 0.5 / 2) + sigmoid(a[1] * 0.5 / 2) + 0.5 + 0.5) / 4
+        assert r[0, 0] == pytest.approx(expect0, abs=1e-15)
+        assert r[0, 1] == pytest.approx(1 - expect0, abs=1e-15)
+
+    def test_layers_mean_and_query_token_sum(self):
+        # L=2, n_q=2, Hq=Hkv=1: R = sum_m mean_l p
+        q = np.zeros((2, 2, 1, 4), np.float32)
+        q[0, 0, 0, 0], q[0, 1, 0, 0], q[1, 0, 0, 0], q[1, 1, 0, 0] = 1.0, -4.0, 6.0, 2.0
+        index = np.zeros((2, 2, 1, 4), np.float32)
+        index[0, :, 0, 0] = [1.0, 0.0]
+        index[1, :, 0, 0] = [0.0, 0.5]
+        r = oracle.block_relevance(q, index, 0, 0)
+        # layer 0 logit gap (b0 - b1) = q/2 ; layer 1 gap = -q*0.5/2
+        e = lambda qa, qb: (sigmoid(qa * 1.0 / 2) + sigmoid(-qb * 0.5 / 2)) / 2
+        expect0 = e(1.0, 6.0) + e(-4.0, 2.0)
+        assert r[0, 0] == pytest.approx(expect0, abs=1e-15)
+        assert r[0, 0] + r[0, 1] == pytest.approx(2.0, abs=1e-15)
+
+    def test_group_max(self):
+        q = np.zeros((1, 2, 4, 4), np.float32)
+        a = np.array([[1.0, -3.0, 2.0, 0.5], [-1.0, 4.0, -2.0, 0.25]])
+        q[0, :, :, 0] = a
+        index = idx4([[1.0, -1.0], [0.0, 0.0]])
+        r = oracle.block_relevance(q, index, 0, 0, mode=oracle.MAX_GROUP)
+        assert r.shape == (2, 2)
+        for g, sign in ((0, 1.0), (1, -1.0)):
+            ps0 = [sigmoid(sign * a[m, h] / 2) for m in range(2) for h in (2 * g, 2 * g + 1)]
+            assert r[g, 0] == pytest.approx(max(ps0), abs=1e-15)
+            assert r[g, 1] == pytest.approx(max(1 - p for p in ps0), abs=1e-15)
+
+    def test_explicit_scale(self):
+        q = np.zeros((1, 1, 1, 4), np.float32)
+        q[..., 0] = 2.0
+        index = idx4([[1.0], [0.5]])
+        r = oracle.block_relevance(q, index, 0, 0, scale=1.0)
+        assert r[0, 0] == pytest.approx(sigmoid(1.0), abs=1e-15)
+
+    def test_uniform_keys(self):
+        q = rng(4).standard_normal((1, 3, 8, 16)).astype(np.float32)
+        index = np.broadcast_to(rng(5).standard_normal((1, 1, 2, 16)).astype(np.float32),
+                                (1, 40, 2, 16)).copy()
+        r = oracle.block_relevance(q, index, 2, 3)
+        np.testing.assert_allclose(r[0, 2:37], 3.0 / 35, rtol=0, atol=1e-15)
+
+    def test_mass_sums_to_query_count(self):
+        q = rng(6).standard_normal((2, 3, 8, 32)).astype(np.float32) * 3
+        index = rng(7).standard_normal((2, 300, 2, 32)).astype(np.float32)
+        r = oracle.block_relevance(q, index, 4, 10)
+        assert np.isinf(r[0, :4]).all() and np.isinf(r[0, 290:]).all()
+        assert r[0, 4:290].sum() == pytest.approx(3.0, abs=1e-12)
+
+    def test_reserved_blocks_outside_softmax(self):
+        q = rng(8).standard_normal((1, 1, 4, 16)).astype(np.float32)
+        index = rng(9).standard_normal((1, 50, 2, 16)).astype(np.float32)
+        r1 = oracle.block_relevance(q, index, 3, 5)
+        index2 = index.copy()
+        index2[0, :3] *= 50.0
+        index2[0, 45:] *= -30.0
+        r2 = oracle.block_relevance(q, index2, 3, 5)
+        np.testing.assert_array_equal(r1, r2)
+
+    def test_single_head_rank_follows_logits(self):
+        q = rng(10).standard_normal((1, 1, 1, 64)).astype(np.float32)
+        index = rng(11).standard_normal((1, 500, 1, 64)).astype(np.float32)
+        r = oracle.block_relevance(q, index, 0, 0)[0]
+        logits = index[0, :, 0, :].astype(np.float64) @ q[0, 0, 0].astype(np.float64)
+        assert list(np.argsort(-r, kind="stable")) == list(np.argsort(-logits, kind="stable"))
+
+
+# ------------------------------------------------------------ selector ---
+def brute_force_select(r32, lo, hi, k):
+    """Max-sum k-subset of candidates; among equal sums the lexicographically smallest ids."""
+    best = None
+    for comb in itertools.combinations(range(lo, hi), k):
+        s = sum(Fraction(float(r32[b])) for b in comb)
+        key = (-s, comb)
+        if best is None or key < best:
+            best = key
+    return list(best[1]) if best else []
+
+
+class TestSelect:
+    @pytest.mark.parametrize("seed", range(6))
+    def test_brute_force_with_ties(self, seed):
+        g = rng(100 + seed)
+        m, s, rr = 12, int(g.integers(0, 3)), int(g.integers(0, 3))
+        r = g.integers(0, 4, m).astype(np.float64)  # many exact ties
+        k = int(g.integers(0, m - s - rr + 1))
+        b2p = g.permutation(m).astype(np.int32)
+        vb, vp = oracle.select(r[None], s, rr, k, b2p)
+        chosen = brute_force_select(r.astype(np.float32), s, m - rr, k)
+        expect = list(range(s)) + chosen + list(range(m - rr, m))
+        assert vb[0].tolist() == expect
+        assert vp[0].tolist() == [int(b2p[b]) for b in expect]
+
+    def test_decision_in_fp32(self):
+        # differ only below fp32 resolution: a tie, so the lower id wins
+        r = np.array([[1.0, 1.0 + 1e-12, 0.5]])
+        vb, _ = oracle.select(r, 0, 0, 1, np.arange(3, dtype=np.int32))
+        assert vb[0].tolist() == [0]
+
+    def test_all_and_none(self):
+        r = rng(12).random((1, 20))
+        b2p = np.arange(20, dtype=np.int32)
+        assert oracle.select(r, 2, 3, 15, b2p)[0][0].tolist() == list(range(20))
+        assert oracle.select(r, 2, 3, 0, b2p)[0][0].tolist() == [0, 1, 17, 18, 19]
+
+    def test_rows_independent(self):
+        r = rng(13).random((3, 30))
+        b2p = rng(14).permutation(30).astype(np.int32)
+        vb, vp = oracle.select(r, 1, 2, 7, b2p)
+        for s in range(3):
+            vb1, vp1 = oracle.select(r[s:s + 1], 1, 2, 7, b2p)
+            assert vb[s].tolist() == vb1[0].tolist() and vp[s].tolist() == vp1[0].tolist()
+            top = sorted(range(1, 28), key=lambda b: (-np.float32(r[s, b]), b))[:7]
+            assert vb[s].tolist() == [0] + sorted(top) + [28, 29]
+
+
+# ----------------------------------------------------------- attention ---
+def sdpa(q, k, v, scale):
+    """torch scaled_dot_product_attention in float64: q [H][d], k/v [H][T][d]."""
+    qt = torch.from_numpy(np.asarray(q, np.float64))[None, :, None, :]
+    kt = torch.from_numpy(np.asarray(k, np.float64))[None]
+    vt = torch.from_numpy(np.asarray(v, np.float64))[None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)
+    lse = torch.logsumexp(scale * (kt @ qt.transpose(-1, -2))[..., 0], dim=-1)
+    return o[0, :, 0, :].numpy(), lse[0].numpy()
+
+
+def widen(pool):
+    return W.bf16_to_f32(pool) if pool.dtype == np.uint16 else pool
+
+
+def gather(pool, pages, g, last=None):
+    """Dense [T][d] keys of KV head g over a page list (last page cut to `last` tokens)."""
+    rows = [widen(pool)[p, g] for p in pages]
+    if last is not None:
+        rows[-1] = rows[-1][:last]
+    return np.concatenate(rows, 0).astype(np.float64)
+
+
+def rand_pools(seed, p, hkv, bt, d, bf16):
+    g = rng(seed)
+    k = g.standard_normal((p, hkv, bt, d)).astype(np.float32)
+    v = g.standard_normal((p, hkv, bt, d)).astype(np.float32)
+    if bf16:
+        return W.bf16_bits(k), W.bf16_bits(v)
+    return k, v
+
+
+class TestAttention:
+    def test_single_token(self):
+        k, v = rand_pools(20, 3, 1, 4, 8, False)
+        q = rng(21).standard_normal((1, 2, 8)).astype(np.float32)
+        out, lse = oracle.view_attention(q, k, v, np.array([[2]], np.int32), last_page_tokens=1)
+        for h in range(2):
+            np.testing.assert_array_equal(out[0, h], v[2, 0, 0].astype(np.float64))
+            a = float(np.dot(q[0, h].astype(np.float64), k[2, 0, 0].astype(np.float64))) / math.sqrt(8)
+            assert lse[0, h] == pytest.approx(a, abs=1e-12)
+
+    def test_identical_keys_average_values(self):
+        k, v = rand_pools(22, 4, 1, 8, 16, False)
+        k[:] = k[0, 0, 0]
+        q = rng(23).standard_normal((2, 1, 16)).astype(np.float32)
+        pages = np.array([[3, 1, 2]], np.int32)
+        out, lse = oracle.view_attention(q, k, v, pages)
+        mean_v = np.concatenate([v[p, 0] for p in (3, 1, 2)], 0).astype(np.float64).mean(0)
+        for m in range(2):
+            np.testing.assert_allclose(out[m, 0], mean_v, rtol=0, atol=1e-14)
+            a = float(np.dot(q[m, 0].astype(np.float64), k[0, 0, 0].astype(np.float64))) / 4.0
+            assert lse[m, 0] == pytest.approx(a + math.log(24), abs=1e-12)
+
+    @pytest.mark.parametrize("bf16", [False, True])
+    @pytest.mark.parametrize("n_sel", [1, 2])
+    def test_matches_torch_sdpa(self, bf16, n_sel):
+        p, hkv, bt, d, hq, nq = 40, 2, 16, 32, 8, 2
+        k, v = rand_pools(24 + bf16, p, hkv, bt, d, bf16)
+        q = rng(26).standard_normal((nq, hq, d)).astype(np.float32)
+        pages = np.stack([rng(27 + s).choice(p, 9, replace=False) for s in range(n_sel)]).astype(np.int32)
+        out, lse = oracle.view_attention(q, k, v, pages, last_page_tokens=5, scale=0.3)
+        for m in range(nq):
+            for h in range(hq):
+                g = h // (hq // hkv)
+                s = 0 if n_sel == 1 else g
+                o_ref, l_ref = sdpa(q[m, h][None], gather(k, pages[s], g, 5)[None],
+                                    gather(v, pages[s], g, 5)[None], 0.3)
+                np.testing.assert_allclose(out[m, h], o_ref[0], rtol=0, atol=1e-12)
+                assert lse[m, h] == pytest.approx(float(l_ref[0]), abs=1e-12)
+
+    @pytest.mark.parametrize("bf16", [False, True])
+    def test_view_equals_masked_dense(self, bf16):
+        m_blocks, hkv, bt, d = 30, 2, 8, 16
+        k, v = rand_pools(30, m_blocks, hkv, bt, d, bf16)
+        q = rng(31).standard_normal((3, 4, d)).astype(np.float32)
+        b2p = rng(32).permutation(m_blocks).astype(np.int32)
+        for n_sel in (1, 2):
+            vb = np.stack([np.sort(rng(33 + s).choice(m_blocks, 11, replace=False))
+                           for s in range(n_sel)]).astype(np.int32)
+            vp = b2p[vb]
+            o1, l1 = oracle.view_attention(q, k, v, vp, last_page_tokens=3)
+            o2, l2 = oracle.masked_dense_attention(q, k, v, b2p, vb, last_page_tokens=3)
+            np.testing.assert_allclose(o1, o2, rtol=0, atol=1e-12)
+            np.testing.assert_allclose(l1, l2, rtol=0, atol=1e-12)
+
+    def test_full_selection_is_full_attention(self):
+        c = W.small_config(history_tokens=1024, recent_tokens=64, n_planted=2, top_k=60)
+        w = W.generate(c, seed=5)
+        index = oracle.mean_k(w.k_pool[0], w.block_to_page)[None]
+        r = oracle.block_relevance(w.q[0], index, 0, c.n_recent)
+        kk = oracle.k_eff(10**9, 10**9, c.block_tokens, c.n_blocks, 0, c.n_recent)
+        assert kk == c.n_candidates
+        vb, vp = oracle.select(r, 0, c.n_recent, kk, w.block_to_page)
+        assert vb[0].tolist() == list(range(c.n_blocks))
+        out, lse = oracle.view_attention(w.q[0, 0], w.k_pool[0], w.v_pool[0], vp)
+        chrono = w.block_to_page  # every block in chronological order
+        for h in range(c.n_q_heads):
+            o_ref, l_ref = sdpa(w.q[0, 0, 0, h][None], gather(w.k_pool[0], chrono, 0)[None],
+                                gather(w.v_pool[0], chrono, 0)[None], 1 / math.sqrt(c.head_dim))
+            np.testing.assert_allclose(out[0, h], o_ref[0], rtol=0, atol=1e-12)
+            assert lse[0, h] == pytest.approx(float(l_ref[0]), abs=1e-12)
+
+
+# ---------------------------------------------------------- generator ---
+class TestWorkload:
+    def test_bf16_rne_against_bit_arithmetic(self):
+        x = np.concatenate([rng(40).standard_normal(10000).astype(np.float32),
+                            # exact ties: low half 0x8000 with even and odd kept lsb
+                            np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x3F80FFFF],
+                                     np.uint32).view(np.float32)])
+        u = x.view(np.uint32).astype(np.uint64)
+        expect = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+        np.testing.assert_array_equal(W.bf16_bits(x), expect)
+        np.testing.assert_array_equal(W.bf16_to_f32(expect[:4]).view(np.uint32),
+                                      expect[:4].astype(np.uint32) << 16)
+
+    def test_deterministic(self):
+        a = W.generate("tiny", seed=9)
+        b = W.generate("tiny", seed=9)
+        np.testing.assert_array_equal(a.k_pool[0], b.k_pool[0])
+        np.testing.assert_array_equal(a.v_pool[0], b.v_pool[0])
+        np.testing.assert_array_equal(a.q, b.q)
+        np.testing.assert_array_equal(a.block_to_page, b.block_to_page)
+        c = W.generate("tiny", seed=10)
+        assert not np.array_equal(a.k_pool[0], c.k_pool[0])
+
+    def test_planted_keys_are_aligned(self):
+        w = W.generate("tiny", seed=0)
+        c = w.cfg
+        u = w.q[0, 0, :, :, :].reshape(-1, c.head_dim).astype(np.float64).mean(0)
+        u /= np.linalg.norm(u)
+        assert len(w.planted) == c.n_planted
+        assert np.all((w.planted >= 0) & (w.planted < c.n_blocks - c.n_recent))
+        for b in w.planted:
+            keys = w.k_pool[0][w.block_to_page[b], 0].astype(np.float64)
+            cos = keys @ u / np.linalg.norm(keys, axis=1)
+            assert np.all(np.abs(cos - 0.9) < 1e-5)
+            assert np.allclose(np.linalg.norm(keys, axis=1), math.sqrt(c.head_dim), rtol=1e-5)
+
+    def test_planted_blocks_are_selected(self):
+        # sanity of the synthetic recipe, not parity: the planted blocks win the selection
+        for seed in range(3):
+            w = W.generate("tiny", seed=seed)
+            c = w.cfg
+            index = oracle.mean_k(w.k_pool[0], w.block_to_page)[None]
+            r = oracle.block_relevance(w.q[0], index, 0, c.n_recent)
+            vb, _ = oracle.select(r, 0, c.n_recent, c.top_k, w.block_to_page)
+            assert set(w.planted.tolist()) <= set(vb[0].tolist())
