@@ -1,0 +1,210 @@
+/*
+ * kvmem.h -- C ABI of the MI355X (gfx950) KVMem decode-step library.
+ *
+ * KVMem (arXiv 2609.04852) keeps an agent's overflowed history as paged KV and,
+ * at each recall point, materializes a bounded execution view: it summarizes
+ * every history block by the mean of its position-independent keys (Eq. 9),
+ * scores every candidate block against the current query with a per-head
+ * softmax over blocks (Eq. 10), keeps the configured sink and recent blocks,
+ * fills the rest of the active budget (Eq. 5, Eq. 7) with the highest-scoring
+ * blocks in chronological order (Sec. 4.3), and runs attention over that view
+ * through a page table (Sec. 4.4, Sec. 5.3).  This library implements that
+ * path on one GPU with every step in HIP kernels:
+ *
+ *   kvmem_build_index  Eq. 9   Mean-K index rows for a range of blocks
+ *   kvmem_select       Eq. 10 + selector: scores, top-k under the budget,
+ *                      chronological view tables
+ *   kvmem_sparse_attn  decode attention over the view's pages (split-K)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Pointers marked "dev" are device pointers, "host" are host
+ * pointers.  Every pointer is borrowed: the library never allocates or frees
+ * memory.  Scratch space is passed in as `workspace`, sized by the matching
+ * *_workspace_bytes query.  All arrays are dense, row-major (C order), and
+ * device arrays must be 16-byte aligned.
+ *
+ * Layouts.  Hkv = n_kv_heads, Hq = n_q_heads (a multiple of Hkv, G = Hq/Hkv),
+ * d = head_dim, Bt = block_tokens (one history block occupies one page):
+ *   K/V page pool  [n_pages][Hkv][Bt][d]      kv_dtype (f32, or bf16 bits)
+ *   Mean-K index   [n_layers][M][Hkv][d]      float, M = history blocks
+ *   query          [n_layers][n_q][Hq][d]     float, position independent
+ *   block_to_page  [M]                        int32, history block -> page
+ *   view tables    [n_sel][n_view]            int32
+ * Query head h attends through KV head floor(h / G).
+ *
+ * Streams.  Every call enqueues its kernels on `stream` (a hipStream_t, NULL
+ * for the null stream) and returns without synchronizing; buffers must stay
+ * valid until that work completes.  No call copies data between host and
+ * device, so a decode step needs no host synchronization.
+ *
+ * Errors.  Arguments are checked on the host before any HIP call.  On an error
+ * nothing is enqueued, no output is written, and kvmem_last_error() describes
+ * the problem.  A failed launch returns KVMEM_ERR_HIP.  Device-side contents
+ * cannot be checked on the host: a page id outside [0, n_pages) is never
+ * dereferenced; the outputs that depend on it are set to NaN instead.
+ *
+ * Determinism.  Identical inputs give bitwise-identical outputs (fixed-order
+ * reductions; integer atomics only).  Calls that share a workspace must not
+ * overlap in time.
+ */
+#ifndef KVMEM_H
+#define KVMEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KVMEM_OK = 0,
+    KVMEM_ERR_NULL = -1,        /* a required pointer is NULL */
+    KVMEM_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
+    KVMEM_ERR_DTYPE = -3,       /* unknown kv_dtype */
+    KVMEM_ERR_UNSUPPORTED = -4, /* valid, but not a shape this build handles */
+    KVMEM_ERR_BUDGET = -5,      /* active budget cannot hold sink + recent (Eq. 7) */
+    KVMEM_ERR_WORKSPACE = -6,   /* workspace missing or smaller than required */
+    KVMEM_ERR_ALIGN = -7,       /* a device pointer is not 16-byte aligned */
+    KVMEM_ERR_HIP = -8          /* a HIP runtime call or kernel launch failed */
+} kvmem_status;
+
+typedef enum { KVMEM_F32 = 0, KVMEM_BF16 = 1 } kvmem_dtype;
+
+/* How Eq. 10's per-(layer, query token, query head) block softmaxes are
+ * combined into selection scores. */
+typedef enum {
+    /* Eq. 10 as printed: R_b = sum_m mean_{l,h} softmax_{b' in C}(...)_b.
+     * One selection shared by every KV head (n_sel = 1). */
+    KVMEM_REDUCE_MEAN_ALL = 0,
+    /* One selection per (layer, KV head): R[l][g][b] = max over the query
+     * tokens m and the query heads h of group g of the same softmax values.
+     * n_sel = n_layers * Hkv. */
+    KVMEM_REDUCE_MAX_GROUP = 1
+} kvmem_reduce;
+
+/* Model geometry shared by all calls.  Supported: Hkv a power of two <= 64,
+ * G = Hq/Hkv with G * n_q <= 16, d in {64, 128}, Bt in {16, 32, 64}. */
+typedef struct {
+    int32_t n_kv_heads;   /* Hkv */
+    int32_t n_q_heads;    /* Hq */
+    int32_t head_dim;     /* d */
+    int32_t block_tokens; /* Bt, tokens per block and per page (Sec. 3.1, Sec. 5.2) */
+    int32_t kv_dtype;     /* kvmem_dtype of the K/V pools */
+} kvmem_geom;
+
+/* Mean-K retrieval index (Eq. 9; Sec. 4.3 "Mean-K Retrieval-Index
+ * Construction", Sec. 5.3 "Incremental Indexing").
+ *
+ * For every block b in [first_block, first_block + n_blocks) and KV head g:
+ *   index[b][g][j] = (1/Bt) * sum_{t < Bt} K[block_to_page[b]][g][t][j],
+ * summed exactly (fp64) and rounded once to fp32, so the result does not depend
+ * on summation order.  Keys are taken as position independent (any RoPE already
+ * removed by the caller).  Call it once per layer, with that layer's pool and
+ * index; it only writes the rows of the given range, so completed blocks can be
+ * indexed incrementally while their keys are resident.
+ *
+ *   k_pool         dev  [n_pages][Hkv][Bt][d] kv_dtype
+ *   n_pages             number of pages in k_pool (> 0)
+ *   block_to_page  dev  int32, read at [first_block, first_block + n_blocks)
+ *   index          dev  float [>= first_block + n_blocks][Hkv][d]
+ *   stream              hipStream_t
+ * n_blocks == 0 is a no-op.  A page id outside [0, n_pages) yields a NaN row. */
+kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
+                               const int32_t *block_to_page, int32_t first_block,
+                               int32_t n_blocks, float *index, void *stream);
+
+/* View plan (Eq. 5, Eq. 7; host only, no HIP call).  With the active budget
+ * B_a = min(model_ctx_tokens, gpu_kv_tokens) and the mandatory context of
+ * (n_sink + n_recent) * Bt tokens,
+ *   k_eff  = min(floor((B_a - (n_sink + n_recent) * Bt) / Bt), M - n_sink - n_recent)
+ *   n_view = n_sink + k_eff + n_recent.
+ * Returns KVMEM_ERR_BUDGET when B_a is below the mandatory context.  k_eff and
+ * n_view (host) may each be NULL. */
+kvmem_status kvmem_plan_view(const kvmem_geom *geom, int32_t n_blocks, int32_t n_sink_blocks,
+                             int32_t n_recent_blocks, int64_t model_ctx_tokens,
+                             int64_t gpu_kv_tokens, int32_t *k_eff, int32_t *n_view);
+
+/* Bytes of workspace kvmem_select needs for these sizes (0 on invalid input). */
+size_t kvmem_select_workspace_bytes(const kvmem_geom *geom, int32_t n_layers, int32_t n_q_tokens,
+                                    int32_t n_blocks, int32_t n_sink_blocks,
+                                    int32_t n_recent_blocks, int32_t mode);
+
+/* Query-conditioned block selection (Eq. 10 and the default selector of
+ * Sec. 4.3; budget from Eq. 5 / Eq. 7).
+ *
+ * The candidate set is C = [n_sink, M - n_recent): the sink blocks [0, n_sink)
+ * and the recent blocks [M - n_recent, M) are always kept and are not part of
+ * the softmax.  For every layer l, query token m and query head h,
+ *   p_{l,m,h,b} = softmax_{b' in C}( scale * q[l][m][h] . index[l][b'][h/G] )_b
+ * then R combines them as `mode` states.  The k_eff candidates with the largest
+ * fp32 R are selected (ties: lower block id first) and the view is emitted in
+ * chronological order:
+ *   view_blocks[s] = [0 .. n_sink) ++ ascending(selected) ++ [M - n_recent .. M)
+ *   view_pages[s][i] = block_to_page[view_blocks[s][i]]
+ *
+ *   q              dev  float [n_layers][n_q][Hq][d]
+ *   index          dev  float [n_layers][M][Hkv][d]
+ *   n_blocks            M; requires n_sink + n_recent < M and |C| <= 65536
+ *   model_ctx_tokens, gpu_kv_tokens   B_model and B_gpu of Eq. 5
+ *   mode                kvmem_reduce
+ *   scale               logit scale; <= 0 selects 1/sqrt(d)
+ *   block_to_page  dev  int32 [M]
+ *   view_blocks    dev  int32 [n_sel][n_view]  (n_sel = 1, or n_layers*Hkv)
+ *   view_pages     dev  int32 [n_sel][n_view]
+ *   scores         dev  float [n_sel][M] or NULL: R per block, rounded to
+ *                       fp32; reserved blocks hold +inf
+ *   n_view_out     host int32 or NULL: receives n_view (known before launch)
+ *   workspace      dev  >= kvmem_select_workspace_bytes(...)
+ *   stream              hipStream_t */
+kvmem_status kvmem_select(const kvmem_geom *geom, int32_t n_layers, const float *q,
+                          int32_t n_q_tokens, const float *index, int32_t n_blocks,
+                          int32_t n_sink_blocks, int32_t n_recent_blocks,
+                          int64_t model_ctx_tokens, int64_t gpu_kv_tokens, int32_t mode,
+                          float scale, const int32_t *block_to_page, int32_t *view_blocks,
+                          int32_t *view_pages, float *scores, int32_t *n_view_out,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace kvmem_sparse_attn needs for these sizes (0 on invalid input). */
+size_t kvmem_sparse_attn_workspace_bytes(const kvmem_geom *geom, int32_t n_q_tokens,
+                                         int32_t n_sel, int32_t n_view);
+
+/* Decode attention over the execution view (Sec. 4.4: the view maps the
+ * selected blocks' physical pages through a page table instead of copying
+ * them; Sec. 5.3 "Copy-free execution-view assembly").
+ *
+ * For query token m and query head h, with KV head g = h / G and view row
+ * s = (n_sel == 1 ? 0 : g), the keys are every token of the pages
+ * view_pages[s][0 .. n_view), in that order, except that the final page holds
+ * only last_page_tokens tokens:
+ *   a_t = scale * q[m][h] . K_t,   out[m][h] = sum_t softmax(a)_t V_t,
+ *   lse[m][h] = log sum_t exp(a_t)   (natural log).
+ * The view is split across workgroups (split-K) and the partial results are
+ * merged exactly through their log-sum-exp.  All n_q query tokens attend to the
+ * same view (no mask among them).
+ *
+ *   q              dev  float [n_q][Hq][d]   one layer
+ *   k_pool, v_pool dev  [n_pages][Hkv][Bt][d] kv_dtype
+ *   view_pages     dev  int32 [n_sel][n_view], n_sel = 1 or Hkv
+ *   last_page_tokens    1 .. Bt
+ *   scale               <= 0 selects 1/sqrt(d)
+ *   out            dev  float [n_q][Hq][d]
+ *   lse            dev  float [n_q][Hq] or NULL
+ *   workspace      dev  >= kvmem_sparse_attn_workspace_bytes(...)
+ *   stream              hipStream_t */
+kvmem_status kvmem_sparse_attn(const kvmem_geom *geom, const float *q, int32_t n_q_tokens,
+                               const void *k_pool, const void *v_pool, int64_t n_pages,
+                               const int32_t *view_pages, int32_t n_sel, int32_t n_view,
+                               int32_t last_page_tokens, float scale, float *out, float *lse,
+                               void *workspace, size_t workspace_bytes, void *stream);
+
+/* Description of the last error on the calling thread ("" after success).
+ * Valid until the next call on that thread. */
+const char *kvmem_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVMEM_H */

@@ -1,0 +1,258 @@
+// C ABI of the KVMem HIP library: argument validation (host only, before any
+// HIP call), workspace sizing, and kernel dispatch.  See include/kvmem.h for
+// the contract of every entry point.
+#include "../../include/kvmem.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "kvmem_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+kvmem_status fail(kvmem_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+kvmem_status ok() {
+    g_error.clear();
+    return KVMEM_OK;
+}
+
+bool pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+kvmem_status check_geom(const kvmem_geom *g) {
+    if (!g) return fail(KVMEM_ERR_NULL, "geom is NULL");
+    if (g->n_kv_heads <= 0 || g->n_q_heads <= 0 || g->n_q_heads % g->n_kv_heads != 0)
+        return fail(KVMEM_ERR_SHAPE, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+                    g->n_q_heads, g->n_kv_heads);
+    if (!pow2(g->n_kv_heads) || g->n_kv_heads > 64)
+        return fail(KVMEM_ERR_UNSUPPORTED, "n_kv_heads %d: a power of two <= 64 is required",
+                    g->n_kv_heads);
+    if (g->head_dim != 64 && g->head_dim != 128)
+        return fail(KVMEM_ERR_UNSUPPORTED, "head_dim %d: 64 or 128 is required", g->head_dim);
+    if (g->block_tokens != 16 && g->block_tokens != 32 && g->block_tokens != 64)
+        return fail(KVMEM_ERR_UNSUPPORTED, "block_tokens %d: 16, 32 or 64 is required",
+                    g->block_tokens);
+    if (g->kv_dtype != KVMEM_F32 && g->kv_dtype != KVMEM_BF16)
+        return fail(KVMEM_ERR_DTYPE, "kv_dtype %d is not KVMEM_F32 or KVMEM_BF16", g->kv_dtype);
+    return KVMEM_OK;
+}
+
+kvmem_status plan_view(const kvmem_geom *g, int32_t n_blocks, int32_t n_sink, int32_t n_recent,
+                       int64_t model_ctx, int64_t gpu_kv, int32_t *k_eff, int32_t *n_view) {
+    if (n_blocks <= 0 || n_sink < 0 || n_recent < 0 || (int64_t)n_sink + n_recent >= n_blocks)
+        return fail(KVMEM_ERR_SHAPE,
+                    "need n_blocks > 0, n_sink >= 0, n_recent >= 0 and n_sink + n_recent < n_blocks "
+                    "(got %d, %d, %d)", n_blocks, n_sink, n_recent);
+    const int64_t b_a = model_ctx < gpu_kv ? model_ctx : gpu_kv;  // Eq. 5
+    const int64_t mandatory = ((int64_t)n_sink + n_recent) * g->block_tokens;
+    if (b_a < mandatory)
+        return fail(KVMEM_ERR_BUDGET, "active budget %lld tokens is below the %lld mandatory sink+recent tokens",
+                    (long long)b_a, (long long)mandatory);
+    const int64_t n_cand = (int64_t)n_blocks - n_sink - n_recent;
+    int64_t k = (b_a - mandatory) / g->block_tokens;  // Eq. 7
+    if (k > n_cand) k = n_cand;
+    if (k_eff) *k_eff = (int32_t)k;
+    if (n_view) *n_view = (int32_t)(n_sink + k + n_recent);
+    return KVMEM_OK;
+}
+
+kvmem_status make_select_plan(const kvmem_geom *g, int32_t n_layers, int32_t n_q, int32_t n_blocks,
+                              int32_t n_sink, int32_t n_recent, int64_t model_ctx, int64_t gpu_kv,
+                              int32_t mode, kvmem::SelectPlan &p) {
+    kvmem_status st = check_geom(g);
+    if (st != KVMEM_OK) return st;
+    if (n_layers <= 0 || n_q <= 0)
+        return fail(KVMEM_ERR_SHAPE, "n_layers (%d) and n_q_tokens (%d) must be positive", n_layers, n_q);
+    if (mode != KVMEM_REDUCE_MEAN_ALL && mode != KVMEM_REDUCE_MAX_GROUP)
+        return fail(KVMEM_ERR_SHAPE, "mode %d is not a kvmem_reduce value", mode);
+    const int group = g->n_q_heads / g->n_kv_heads;
+    const int rows = group * n_q;
+    if (!pow2(rows) || rows > 16)
+        return fail(KVMEM_ERR_UNSUPPORTED,
+                    "G * n_q_tokens = %d: scoring needs a power of two <= 16", rows);
+    int32_t k_eff = 0, n_view = 0;
+    st = plan_view(g, n_blocks, n_sink, n_recent, model_ctx, gpu_kv, &k_eff, &n_view);
+    if (st != KVMEM_OK) return st;
+    const int32_t n_cand = n_blocks - n_sink - n_recent;
+    if (n_cand > kvmem::kTopkMaxCand)
+        return fail(KVMEM_ERR_UNSUPPORTED, "%d candidate blocks: at most %d are supported", n_cand,
+                    kvmem::kTopkMaxCand);
+    if ((int64_t)n_layers * n_q * g->n_q_heads > (1 << 20))
+        return fail(KVMEM_ERR_UNSUPPORTED, "too many query rows");
+    p = kvmem::SelectPlan{};
+    p.n_layers = n_layers;
+    p.n_q = n_q;
+    p.n_q_heads = g->n_q_heads;
+    p.n_kv_heads = g->n_kv_heads;
+    p.head_dim = g->head_dim;
+    p.group = group;
+    p.rows_per_head = rows;
+    p.n_blocks = n_blocks;
+    p.n_sink = n_sink;
+    p.n_recent = n_recent;
+    p.n_cand = n_cand;
+    p.k_eff = k_eff;
+    p.n_view = n_view;
+    p.mode = mode;
+    p.n_sel = mode == KVMEM_REDUCE_MEAN_ALL ? 1 : n_layers * g->n_kv_heads;
+    kvmem::plan_select_layout(p);
+    return KVMEM_OK;
+}
+
+kvmem_status make_attn_plan(const kvmem_geom *g, int32_t n_q, int32_t n_sel, int32_t n_view,
+                            int32_t last_page_tokens, kvmem::AttnPlan &p) {
+    kvmem_status st = check_geom(g);
+    if (st != KVMEM_OK) return st;
+    if (n_q <= 0) return fail(KVMEM_ERR_SHAPE, "n_q_tokens %d must be positive", n_q);
+    if (n_sel != 1 && n_sel != g->n_kv_heads)
+        return fail(KVMEM_ERR_SHAPE, "n_sel %d must be 1 or n_kv_heads (%d)", n_sel, g->n_kv_heads);
+    if (n_view <= 0) return fail(KVMEM_ERR_SHAPE, "n_view %d must be positive", n_view);
+    if (last_page_tokens < 1 || last_page_tokens > g->block_tokens)
+        return fail(KVMEM_ERR_SHAPE, "last_page_tokens %d must be in [1, %d]", last_page_tokens,
+                    g->block_tokens);
+    const int group = g->n_q_heads / g->n_kv_heads;
+    if ((int64_t)group * n_q > 4096) return fail(KVMEM_ERR_UNSUPPORTED, "too many query rows per KV head");
+    p = kvmem::AttnPlan{};
+    p.n_kv_heads = g->n_kv_heads;
+    p.n_q_heads = g->n_q_heads;
+    p.group = group;
+    p.n_q = n_q;
+    p.rows_per_head = group * n_q;
+    p.head_dim = g->head_dim;
+    p.block_tokens = g->block_tokens;
+    p.kv_dtype = g->kv_dtype;
+    p.n_sel = n_sel;
+    p.n_view = n_view;
+    p.last_page_tokens = last_page_tokens;
+    kvmem::plan_attn_layout(p);
+    return KVMEM_OK;
+}
+
+kvmem_status hip_status(hipError_t e, const char *what) {
+    if (e == hipSuccess) return ok();
+    return fail(KVMEM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kvmem_last_error(void) { return g_error.c_str(); }
+
+kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
+                               const int32_t *block_to_page, int32_t first_block,
+                               int32_t n_blocks, float *index, void *stream) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    if (first_block < 0 || n_blocks < 0 || (int64_t)first_block + n_blocks > INT32_MAX)
+        return fail(KVMEM_ERR_SHAPE, "block range [%d, %d + %d) is invalid", first_block, first_block,
+                    n_blocks);
+    if (n_blocks == 0) return ok();
+    if (!k_pool || !block_to_page || !index)
+        return fail(KVMEM_ERR_NULL, "k_pool, block_to_page and index must be non-NULL");
+    if (n_pages <= 0) return fail(KVMEM_ERR_SHAPE, "n_pages %lld must be positive", (long long)n_pages);
+    if (!aligned16(k_pool) || !aligned16(index) || !aligned16(block_to_page))
+        return fail(KVMEM_ERR_ALIGN, "k_pool, block_to_page and index must be 16-byte aligned");
+    return hip_status(kvmem::launch_build_index(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
+                                                geom->block_tokens, k_pool, n_pages, block_to_page,
+                                                first_block, n_blocks, index,
+                                                static_cast<hipStream_t>(stream)),
+                      "build_index launch");
+}
+
+kvmem_status kvmem_plan_view(const kvmem_geom *geom, int32_t n_blocks, int32_t n_sink_blocks,
+                             int32_t n_recent_blocks, int64_t model_ctx_tokens,
+                             int64_t gpu_kv_tokens, int32_t *k_eff, int32_t *n_view) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    st = plan_view(geom, n_blocks, n_sink_blocks, n_recent_blocks, model_ctx_tokens, gpu_kv_tokens,
+                   k_eff, n_view);
+    return st == KVMEM_OK ? ok() : st;
+}
+
+size_t kvmem_select_workspace_bytes(const kvmem_geom *geom, int32_t n_layers, int32_t n_q_tokens,
+                                    int32_t n_blocks, int32_t n_sink_blocks,
+                                    int32_t n_recent_blocks, int32_t mode) {
+    kvmem::SelectPlan p;
+    // the budget does not change the workspace; use the largest one
+    if (make_select_plan(geom, n_layers, n_q_tokens, n_blocks, n_sink_blocks, n_recent_blocks,
+                         INT64_MAX, INT64_MAX, mode, p) != KVMEM_OK)
+        return 0;
+    ok();
+    return p.total;
+}
+
+kvmem_status kvmem_select(const kvmem_geom *geom, int32_t n_layers, const float *q,
+                          int32_t n_q_tokens, const float *index, int32_t n_blocks,
+                          int32_t n_sink_blocks, int32_t n_recent_blocks,
+                          int64_t model_ctx_tokens, int64_t gpu_kv_tokens, int32_t mode,
+                          float scale, const int32_t *block_to_page, int32_t *view_blocks,
+                          int32_t *view_pages, float *scores, int32_t *n_view_out,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+    kvmem::SelectPlan p;
+    kvmem_status st = make_select_plan(geom, n_layers, n_q_tokens, n_blocks, n_sink_blocks,
+                                       n_recent_blocks, model_ctx_tokens, gpu_kv_tokens, mode, p);
+    if (st != KVMEM_OK) return st;
+    if (!q || !index || !block_to_page || !view_blocks || !view_pages)
+        return fail(KVMEM_ERR_NULL, "q, index, block_to_page, view_blocks and view_pages must be non-NULL");
+    if (!workspace || workspace_bytes < p.total)
+        return fail(KVMEM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required",
+                    workspace_bytes, p.total);
+    if (!aligned16(q) || !aligned16(index) || !aligned16(block_to_page) || !aligned16(view_blocks) ||
+        !aligned16(view_pages) || (scores && !aligned16(scores)) || !aligned16(workspace))
+        return fail(KVMEM_ERR_ALIGN, "device pointers must be 16-byte aligned");
+    if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)geom->head_dim);
+    if (n_view_out) *n_view_out = p.n_view;
+    return hip_status(kvmem::launch_select(p, q, index, scale, block_to_page, view_blocks, view_pages,
+                                           scores, static_cast<char *>(workspace),
+                                           static_cast<hipStream_t>(stream)),
+                      "select launch");
+}
+
+size_t kvmem_sparse_attn_workspace_bytes(const kvmem_geom *geom, int32_t n_q_tokens, int32_t n_sel,
+                                         int32_t n_view) {
+    kvmem::AttnPlan p;
+    if (make_attn_plan(geom, n_q_tokens, n_sel, n_view, 1, p) != KVMEM_OK) return 0;
+    ok();
+    return p.total;
+}
+
+kvmem_status kvmem_sparse_attn(const kvmem_geom *geom, const float *q, int32_t n_q_tokens,
+                               const void *k_pool, const void *v_pool, int64_t n_pages,
+                               const int32_t *view_pages, int32_t n_sel, int32_t n_view,
+                               int32_t last_page_tokens, float scale, float *out, float *lse,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+    kvmem::AttnPlan p;
+    kvmem_status st = make_attn_plan(geom, n_q_tokens, n_sel, n_view, last_page_tokens, p);
+    if (st != KVMEM_OK) return st;
+    if (!q || !k_pool || !v_pool || !view_pages || !out)
+        return fail(KVMEM_ERR_NULL, "q, k_pool, v_pool, view_pages and out must be non-NULL");
+    if (n_pages <= 0) return fail(KVMEM_ERR_SHAPE, "n_pages %lld must be positive", (long long)n_pages);
+    if (!workspace || workspace_bytes < p.total)
+        return fail(KVMEM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required",
+                    workspace_bytes, p.total);
+    if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(view_pages) ||
+        !aligned16(out) || (lse && !aligned16(lse)) || !aligned16(workspace))
+        return fail(KVMEM_ERR_ALIGN, "device pointers must be 16-byte aligned");
+    if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)geom->head_dim);
+    return hip_status(kvmem::launch_sparse_attn(p, q, k_pool, v_pool, n_pages, view_pages, scale, out,
+                                                lse, static_cast<char *>(workspace),
+                                                static_cast<hipStream_t>(stream)),
+                      "sparse_attn launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,235 @@
+"""Python binding of the KVMem C ABI (libkvmem.so): argument marshalling only.
+
+Each function has the name of the C entry point it calls and takes torch
+tensors for device buffers; every step of the computation runs in the HIP
+kernels behind the C ABI.  The library is loaded on first use and an
+ImportError is raised if it has not been built -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import re
+
+import torch
+
+KVMEM_OK = 0
+KVMEM_F32, KVMEM_BF16 = 0, 1
+KVMEM_REDUCE_MEAN_ALL, KVMEM_REDUCE_MAX_GROUP = 0, 1
+
+STATUS_NAMES = {
+    0: "KVMEM_OK", -1: "KVMEM_ERR_NULL", -2: "KVMEM_ERR_SHAPE", -3: "KVMEM_ERR_DTYPE",
+    -4: "KVMEM_ERR_UNSUPPORTED", -5: "KVMEM_ERR_BUDGET", -6: "KVMEM_ERR_WORKSPACE",
+    -7: "KVMEM_ERR_ALIGN", -8: "KVMEM_ERR_HIP",
+}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvmem.so")
+HEADER_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                           "include", "kvmem.h")
+
+
+class KvmemError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class kvmem_geom(ctypes.Structure):
+    _fields_ = [("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_tokens", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32)]
+
+
+@dataclasses.dataclass(frozen=True)
+class Geom:
+    n_kv_heads: int
+    n_q_heads: int
+    head_dim: int
+    block_tokens: int
+    kv_dtype: int  # KVMEM_F32 or KVMEM_BF16
+
+    def c(self) -> kvmem_geom:
+        return kvmem_geom(self.n_kv_heads, self.n_q_heads, self.head_dim, self.block_tokens,
+                          self.kv_dtype)
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libkvmem.so (raises ImportError if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_04852_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, G = ctypes.c_void_p, ctypes.POINTER(kvmem_geom)
+    i32, i64, f32, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    L.kvmem_build_index.argtypes = [G, P, i64, P, i32, i32, P, P]
+    L.kvmem_plan_view.argtypes = [G, i32, i32, i32, i64, i64, pi32, pi32]
+    L.kvmem_select_workspace_bytes.argtypes = [G, i32, i32, i32, i32, i32, i32]
+    L.kvmem_select_workspace_bytes.restype = sz
+    L.kvmem_select.argtypes = [G, i32, P, i32, P, i32, i32, i32, i64, i64, i32, f32, P, P, P, P,
+                               pi32, P, sz, P]
+    L.kvmem_sparse_attn_workspace_bytes.argtypes = [G, i32, i32, i32]
+    L.kvmem_sparse_attn_workspace_bytes.restype = sz
+    L.kvmem_sparse_attn.argtypes = [G, P, i32, P, P, i64, P, i32, i32, i32, f32, P, P, P, sz, P]
+    for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_sparse_attn"):
+        getattr(L, name).restype = ctypes.c_int
+    L.kvmem_last_error.argtypes = []
+    L.kvmem_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def header_functions() -> list[str]:
+    """Names of the functions declared in include/kvmem.h."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(kvmem_\w+)\s*\(", text, re.M)))
+
+
+def kvmem_last_error() -> str:
+    return lib().kvmem_last_error().decode()
+
+
+def _check(status: int):
+    if status != KVMEM_OK:
+        raise KvmemError(status, kvmem_last_error())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def kv_dtype_of(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return KVMEM_BF16
+    if t.dtype == torch.float32:
+        return KVMEM_F32
+    raise TypeError(f"K/V pools must be bfloat16 or float32, got {t.dtype}")
+
+
+def _need(t: torch.Tensor, dtype, name: str):
+    if t.dtype != dtype or not t.is_contiguous() or not t.is_cuda:
+        raise TypeError(f"{name} must be a contiguous CUDA {dtype} tensor")
+
+
+def kvmem_build_index(geom: Geom, k_pool: torch.Tensor, block_to_page: torch.Tensor,
+                      first_block: int, n_blocks: int, index: torch.Tensor, stream=None):
+    _need(block_to_page, torch.int32, "block_to_page")
+    _need(index, torch.float32, "index")
+    if not k_pool.is_cuda or not k_pool.is_contiguous():
+        raise TypeError("k_pool must be a contiguous CUDA tensor")
+    if block_to_page.numel() < first_block + n_blocks:
+        raise ValueError("block_to_page is shorter than the block range")
+    row = geom.n_kv_heads * geom.head_dim
+    if index.numel() < (first_block + n_blocks) * row:
+        raise ValueError("index is smaller than the block range")
+    n_pages = k_pool.numel() // (geom.n_kv_heads * geom.block_tokens * geom.head_dim)
+    _check(lib().kvmem_build_index(ctypes.byref(geom.c()), _ptr(k_pool), n_pages,
+                                   _ptr(block_to_page), first_block, n_blocks, _ptr(index),
+                                   _stream(stream)))
+
+
+def kvmem_plan_view(geom: Geom, n_blocks: int, n_sink: int, n_recent: int,
+                    model_ctx_tokens: int, gpu_kv_tokens: int) -> tuple[int, int]:
+    k = ctypes.c_int32()
+    n = ctypes.c_int32()
+    _check(lib().kvmem_plan_view(ctypes.byref(geom.c()), n_blocks, n_sink, n_recent,
+                                 model_ctx_tokens, gpu_kv_tokens, ctypes.byref(k), ctypes.byref(n)))
+    return k.value, n.value
+
+
+def kvmem_select_workspace_bytes(geom: Geom, n_layers: int, n_q: int, n_blocks: int, n_sink: int,
+                                 n_recent: int, mode: int) -> int:
+    n = lib().kvmem_select_workspace_bytes(ctypes.byref(geom.c()), n_layers, n_q, n_blocks, n_sink,
+                                           n_recent, mode)
+    if n == 0:
+        raise KvmemError(-2, kvmem_last_error())
+    return n
+
+
+def kvmem_select(geom: Geom, q: torch.Tensor, index: torch.Tensor, n_sink: int, n_recent: int,
+                 model_ctx_tokens: int, gpu_kv_tokens: int, mode: int, scale: float,
+                 block_to_page: torch.Tensor, view_blocks: torch.Tensor, view_pages: torch.Tensor,
+                 workspace: torch.Tensor, scores: torch.Tensor | None = None, stream=None) -> int:
+    """q [L][n_q][Hq][d] float32, index [L][M][Hkv][d] float32.  Returns n_view."""
+    _need(q, torch.float32, "q")
+    _need(index, torch.float32, "index")
+    _need(block_to_page, torch.int32, "block_to_page")
+    _need(view_blocks, torch.int32, "view_blocks")
+    _need(view_pages, torch.int32, "view_pages")
+    _need(workspace, torch.uint8, "workspace")
+    if q.dim() != 4 or index.dim() != 4 or q.shape[0] != index.shape[0]:
+        raise ValueError("q must be [L][n_q][Hq][d] and index [L][M][Hkv][d]")
+    n_layers, n_q = q.shape[0], q.shape[1]
+    n_blocks = index.shape[1]
+    if tuple(q.shape[2:]) != (geom.n_q_heads, geom.head_dim) or \
+            tuple(index.shape[2:]) != (geom.n_kv_heads, geom.head_dim):
+        raise ValueError("q/index shapes do not match the geometry")
+    if block_to_page.numel() != n_blocks:
+        raise ValueError("block_to_page must have one entry per block")
+    k_eff, n_view = kvmem_plan_view(geom, n_blocks, n_sink, n_recent, model_ctx_tokens, gpu_kv_tokens)
+    n_sel = 1 if mode == KVMEM_REDUCE_MEAN_ALL else n_layers * geom.n_kv_heads
+    if view_blocks.numel() < n_sel * n_view or view_pages.numel() < n_sel * n_view:
+        raise ValueError("view tables are smaller than n_sel * n_view")
+    if scores is not None:
+        _need(scores, torch.float32, "scores")
+        if scores.numel() < n_sel * n_blocks:
+            raise ValueError("scores is smaller than n_sel * n_blocks")
+    out_n = ctypes.c_int32()
+    _check(lib().kvmem_select(ctypes.byref(geom.c()), n_layers, _ptr(q), n_q, _ptr(index), n_blocks,
+                              n_sink, n_recent, model_ctx_tokens, gpu_kv_tokens, mode, scale,
+                              _ptr(block_to_page), _ptr(view_blocks), _ptr(view_pages), _ptr(scores),
+                              ctypes.byref(out_n), _ptr(workspace), workspace.numel(),
+                              _stream(stream)))
+    return out_n.value
+
+
+def kvmem_sparse_attn_workspace_bytes(geom: Geom, n_q: int, n_sel: int, n_view: int) -> int:
+    n = lib().kvmem_sparse_attn_workspace_bytes(ctypes.byref(geom.c()), n_q, n_sel, n_view)
+    if n == 0:
+        raise KvmemError(-2, kvmem_last_error())
+    return n
+
+
+def kvmem_sparse_attn(geom: Geom, q: torch.Tensor, k_pool: torch.Tensor, v_pool: torch.Tensor,
+                      view_pages: torch.Tensor, n_sel: int, n_view: int, last_page_tokens: int,
+                      scale: float, out: torch.Tensor, workspace: torch.Tensor,
+                      lse: torch.Tensor | None = None, stream=None):
+    """q [n_q][Hq][d] float32 (one layer); view_pages [n_sel][n_view] int32."""
+    _need(q, torch.float32, "q")
+    _need(out, torch.float32, "out")
+    _need(view_pages, torch.int32, "view_pages")
+    _need(workspace, torch.uint8, "workspace")
+    if k_pool.dtype != v_pool.dtype or k_pool.shape != v_pool.shape:
+        raise ValueError("K and V pools must match in dtype and shape")
+    if kv_dtype_of(k_pool) != geom.kv_dtype:
+        raise TypeError("pool dtype does not match geom.kv_dtype")
+    if not (k_pool.is_cuda and v_pool.is_cuda and k_pool.is_contiguous() and v_pool.is_contiguous()):
+        raise TypeError("pools must be contiguous CUDA tensors")
+    if q.dim() != 3 or tuple(q.shape[1:]) != (geom.n_q_heads, geom.head_dim):
+        raise ValueError("q must be [n_q][Hq][d]")
+    n_q = q.shape[0]
+    if out.numel() != q.numel():
+        raise ValueError("out must have the shape of q")
+    if view_pages.numel() < n_sel * n_view:
+        raise ValueError("view_pages is smaller than n_sel * n_view")
+    if lse is not None:
+        _need(lse, torch.float32, "lse")
+        if lse.numel() < n_q * geom.n_q_heads:
+            raise ValueError("lse is smaller than n_q * Hq")
+    n_pages = k_pool.numel() // (geom.n_kv_heads * geom.block_tokens * geom.head_dim)
+    _check(lib().kvmem_sparse_attn(ctypes.byref(geom.c()), _ptr(q), n_q, _ptr(k_pool), _ptr(v_pool),
+                                   n_pages, _ptr(view_pages), n_sel, n_view, last_page_tokens, scale,
+                                   _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
+                                   _stream(stream)))

@@ -1,0 +1,242 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Inputs come from the seeded generator only; expected values come from the
+oracle only.  Every case prints what it runs before touching the GPU.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_04852_amd import kvmem as K
+from paper_2609_04852_amd import workload as W
+from paper_2609_04852_amd.step import LayerState
+
+from parity import (assert_index_bitwise, check_attention, check_scores, check_selection, log)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    K.lib()  # raises if the library is not built
+    yield
+    torch.cuda.synchronize()
+
+
+def oracle_mode(cfg):
+    return oracle.MEAN_ALL if cfg.mode == W.MEAN_ALL else oracle.MAX_GROUP
+
+
+def run_case(cfg, seed, layer=0, budget=None, lpt=None, e2e=True, stats=None):
+    """Generate, run the oracle and the GPU path for one layer, and compare."""
+    budget = cfg.budget_tokens if budget is None else budget
+    log(f"[case] {cfg.name} seed={seed} layer={layer} M={cfg.n_blocks} Hkv={cfg.n_kv_heads} "
+        f"Hq={cfg.n_q_heads} d={cfg.head_dim} Bt={cfg.block_tokens} {cfg.kv_dtype} n_q={cfg.n_q} "
+        f"S={cfg.sink_blocks} Rr={cfg.n_recent} budget={budget} mode={cfg.mode}")
+    w = W.generate(cfg, seed, layers=layer + 1)
+    kp, vp_pool, b2p = w.k_pool[layer], w.v_pool[layer], w.block_to_page
+    q_l = w.q[0, layer:layer + 1]  # [1][n_q][Hq][d]
+    S, Rr = cfg.sink_blocks, cfg.n_recent
+    # ---- oracle
+    index_ref = oracle.mean_k(kp, b2p)
+    rel = oracle.block_relevance(q_l, index_ref[None], S, Rr, oracle_mode(cfg))
+    k_eff = oracle.k_eff(budget, budget, cfg.block_tokens, cfg.n_blocks, S, Rr)
+    vb_ref, vp_ref = oracle.select(rel, S, Rr, k_eff, b2p)
+    last = cfg.block_tokens if lpt is None else lpt
+    out_ref, lse_ref = oracle.view_attention(q_l[0], kp, vp_pool, vp_ref, last_page_tokens=last)
+    # ---- GPU
+    log("  gpu: build_index")
+    st = LayerState(cfg, kp, vp_pool, b2p, budget_tokens=budget)
+    st.build_index()
+    torch.cuda.synchronize()
+    assert_index_bitwise(st.index[0].cpu().numpy(), index_ref)
+    log("  gpu: select")
+    qd = torch.from_numpy(np.ascontiguousarray(q_l)).cuda()
+    n_view = st.select(qd)
+    torch.cuda.synchronize()
+    assert n_view == S + k_eff + Rr
+    vb, vpg = st.view_blocks.cpu().numpy(), st.view_pages.cpu().numpy()
+    sel_stats = check_selection(vb, vpg, rel, b2p, S, Rr, k_eff, ref_view=vb_ref)
+    worst = check_scores(st.scores.cpu().numpy(), rel, S, Rr)
+    log(f"  selection ok: {sel_stats}, worst score rel err {worst:.2e}")
+    log("  gpu: attention on the oracle's view")
+    out, lse = st.attend(qd[0], torch.from_numpy(vp_ref).cuda(), last_page_tokens=last)
+    torch.cuda.synchronize()
+    err = check_attention(out.cpu().numpy(), lse.cpu().numpy(), out_ref, lse_ref, cfg.kv_dtype)
+    log(f"  attention ok: max abs err out {err[0]:.2e} lse {err[1]:.2e}")
+    if e2e and np.array_equal(vb, vb_ref):
+        log("  gpu: attention on its own view")
+        out2, lse2 = st.attend(qd[0], last_page_tokens=last)
+        torch.cuda.synchronize()
+        check_attention(out2.cpu().numpy(), lse2.cpu().numpy(), out_ref, lse_ref, cfg.kv_dtype)
+    if stats is not None:
+        stats.update(sel_stats)
+    return st, w
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_tiny(seed):
+    run_case(W.CONFIGS["tiny"], seed)
+
+
+@pytest.mark.parametrize("name", ["64k", "256k"])
+def test_mid_configs(name):
+    run_case(W.CONFIGS[name], W.CONFIGS[name].seed)
+
+
+def test_1m():
+    run_case(W.CONFIGS["1m"], W.CONFIGS["1m"].seed)
+
+
+def test_1m_mtp4_layer0():
+    run_case(W.CONFIGS["1m_mtp4"], W.CONFIGS["1m_mtp4"].seed, layer=0)
+
+
+SHAPES = [
+    # Hkv, Hq, d, Bt, dtype, M, S, Rr, n_q, mode, budget blocks beyond sink+recent
+    (2, 8, 128, 32, "f32", 700, 3, 5, 2, W.MEAN_ALL, 100),
+    (4, 4, 64, 64, "bf16", 333, 0, 1, 1, W.MAX_GROUP, 41),
+    (1, 8, 64, 16, "bf16", 1500, 2, 7, 2, W.MAX_GROUP, 230),
+    (8, 16, 128, 16, "bf16", 2000, 0, 33, 4, W.MEAN_ALL, 517),
+    (16, 32, 64, 32, "bf16", 900, 1, 9, 1, W.MEAN_ALL, 77),
+    (32, 64, 128, 16, "bf16", 300, 0, 4, 1, W.MAX_GROUP, 50),
+    (2, 2, 128, 64, "f32", 129, 0, 1, 1, W.MEAN_ALL, 1),
+]
+
+
+def shape_cfg(hkv, hq, d, bt, dt, m, s, rr, nq, mode, extra, planted=3):
+    return W.small_config(n_kv_heads=hkv, n_q_heads=hq, head_dim=d, block_tokens=bt, kv_dtype=dt,
+                          history_tokens=m * bt, recent_tokens=rr * bt, sink_blocks=s,
+                          budget_tokens=(s + rr + extra) * bt, n_q=nq, mode=mode, n_planted=planted)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"s{i}" for i in range(len(SHAPES))])
+def test_shapes(shape):
+    run_case(shape_cfg(*shape), 11)
+
+
+@pytest.mark.parametrize("which", ["none", "all"])
+def test_budget_extremes(which):
+    cfg = shape_cfg(4, 16, 128, 16, "bf16", 600, 2, 6, 1, W.MEAN_ALL, 0)
+    budget = (2 + 6) * 16 if which == "none" else 10**9
+    run_case(cfg, 3, budget=budget)
+
+
+def test_partial_last_page():
+    cfg = shape_cfg(2, 8, 128, 32, "bf16", 400, 0, 3, 2, W.MEAN_ALL, 60)
+    run_case(cfg, 5, lpt=7)
+    run_case(cfg, 6, lpt=1)
+
+
+def test_full_selection_is_dense_attention():
+    cfg = shape_cfg(2, 8, 64, 16, "f32", 300, 1, 2, 1, W.MEAN_ALL, 0)
+    log("[case] full selection vs dense attention")
+    w = W.generate(cfg, 8)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page, budget_tokens=10**9)
+    st.build_index()
+    qd = torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda()
+    st.select(qd)
+    out, lse = st.attend(qd[0])
+    torch.cuda.synchronize()
+    assert st.view_blocks.cpu().numpy()[0].tolist() == list(range(cfg.n_blocks))
+    all_blocks = np.arange(cfg.n_blocks, dtype=np.int32)[None]
+    o_ref, l_ref = oracle.masked_dense_attention(w.q[0, 0], w.k_pool[0], w.v_pool[0], w.block_to_page,
+                                                 all_blocks)
+    check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, "f32")
+
+
+def test_exact_ties_take_lower_ids():
+    """Blocks whose pages hold identical keys score identically; the lower ids win."""
+    cfg = shape_cfg(2, 8, 128, 16, "bf16", 500, 0, 4, 1, W.MEAN_ALL, 40, planted=0)
+    log("[case] exact ties")
+    w = W.generate(cfg, 9)
+    kp = w.k_pool[0].copy()
+    # every page gets the keys of one of 20 source pages: massive exact ties
+    src = np.random.default_rng(0).integers(0, 20, cfg.n_blocks)
+    kp[:] = kp[src]
+    index_ref = oracle.mean_k(kp, w.block_to_page)
+    rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 0, cfg.n_recent)
+    k_eff = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, 16, cfg.n_blocks, 0, cfg.n_recent)
+    vb_ref, _ = oracle.select(rel, 0, cfg.n_recent, k_eff, w.block_to_page)
+    st = LayerState(cfg, kp, w.v_pool[0], w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(st.view_blocks.cpu().numpy(), vb_ref)
+
+
+def test_incremental_index_build():
+    cfg = W.CONFIGS["64k"]
+    log("[case] incremental index build")
+    w = W.generate(cfg, 1, with_values=False)
+    st = LayerState(cfg, w.k_pool[0], None, w.block_to_page)
+    st.index.fill_(-1.0)
+    for lo, hi in [(0, 1000), (1000, 1001), (1001, 4096)]:
+        st.build_index(lo, hi - lo)
+    torch.cuda.synchronize()
+    assert_index_bitwise(st.index[0].cpu().numpy(), oracle.mean_k(w.k_pool[0], w.block_to_page))
+
+
+def test_deterministic():
+    cfg = W.CONFIGS["256k"]
+    log("[case] determinism (two runs)")
+    w = W.generate(cfg, 2)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    qd = torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda()
+    outs = []
+    for _ in range(2):
+        st.build_index()
+        st.select(qd)
+        o, l = st.attend(qd[0])
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy().copy() for t in (st.index, st.scores, st.view_blocks, o, l)])
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def test_random_views_per_head():
+    """Attention alone on arbitrary page lists (one per KV head), any order."""
+    cfg = shape_cfg(4, 16, 128, 32, "bf16", 800, 0, 2, 2, W.MAX_GROUP, 10)
+    log("[case] random per-head views")
+    w = W.generate(cfg, 12)
+    rng = np.random.default_rng(3)
+    vp = np.stack([rng.choice(cfg.n_blocks, 257, replace=False) for _ in range(4)]).astype(np.int32)
+    o_ref, l_ref = oracle.view_attention(w.q[0, 0], w.k_pool[0], w.v_pool[0], vp, last_page_tokens=13)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    qd = torch.from_numpy(np.ascontiguousarray(w.q[0, 0])).cuda()
+    out, lse = st.attend(qd, torch.from_numpy(vp).cuda(), last_page_tokens=13)
+    torch.cuda.synchronize()
+    check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, "bf16")
+
+
+def test_out_of_range_pages_give_nan():
+    """A page id outside the pool is never read; the outputs that need it are NaN."""
+    cfg = shape_cfg(2, 8, 64, 16, "f32", 200, 0, 2, 1, W.MAX_GROUP, 20)
+    log("[case] out-of-range page ids")
+    w = W.generate(cfg, 13)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    qd = torch.from_numpy(np.ascontiguousarray(w.q[0, 0])).cuda()
+    vp = np.stack([np.arange(30), np.arange(30, 60)]).astype(np.int32)
+    vp[1, 17] = cfg.n_blocks + 1000  # only KV head 1 sees the bad page
+    out, lse = st.attend(qd, torch.from_numpy(vp).cuda())
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert np.isnan(o[:, 4:]).all() and np.isfinite(o[:, :4]).all()
+    o_ref, _ = oracle.view_attention(w.q[0, 0, :, :4], w.k_pool[0][:, :1], w.v_pool[0][:, :1], vp[:1])
+    np.testing.assert_allclose(o[:, :4], o_ref, atol=1e-4, rtol=0)
+    b2p = w.block_to_page.copy()
+    b2p[7] = -3
+    st2 = LayerState(cfg, w.k_pool[0], None, b2p)
+    st2.build_index()
+    torch.cuda.synchronize()
+    idx = st2.index[0].cpu().numpy()
+    assert np.isnan(idx[7]).all()
+    ok = np.ones(cfg.n_blocks, bool)
+    ok[7] = False
+    ref = oracle.mean_k(w.k_pool[0], w.block_to_page)
+    assert_index_bitwise(idx[ok], ref[ok])
