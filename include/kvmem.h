@@ -27,7 +27,11 @@
  * Layouts.  Hkv = n_kv_heads, Hq = n_q_heads (a multiple of Hkv, G = Hq/Hkv),
  * d = head_dim, Bt = block_tokens (one history block occupies one page):
  *   K/V page pool  [n_pages][Hkv][Bt][d]      kv_dtype (f32, or bf16 bits)
- *   Mean-K index   [n_layers][M][Hkv][d]      float, M = history blocks
+ *   Mean-K index   [n_layers][T][Hkv][d/4][64][4]  float, tiled: T = ceil(M/64)
+ *                  tiles of 64 blocks, M = history blocks; the entry of block
+ *                  b, KV head g, dimension j is at
+ *                  (((b/64)*Hkv + g)*(d/4) + j/4)*256 + (b%64)*4 + j%4
+ *                  within a layer (kvmem_index_bytes gives a layer's size)
  *   query          [n_layers][n_q][Hq][d]     float, position independent
  *   block_to_page  [M]                        int32, history block -> page
  *   view tables    [n_sel][n_view]            int32
@@ -94,6 +98,10 @@ typedef struct {
     int32_t kv_dtype;     /* kvmem_dtype of the K/V pools */
 } kvmem_geom;
 
+/* Bytes of one layer's Mean-K index for n_blocks history blocks (the tiled
+ * layout rounds the block count up to a multiple of 64).  0 on invalid input. */
+size_t kvmem_index_bytes(const kvmem_geom *geom, int32_t n_blocks);
+
 /* Mean-K retrieval index (Eq. 9; Sec. 4.3 "Mean-K Retrieval-Index
  * Construction", Sec. 5.3 "Incremental Indexing").
  *
@@ -108,7 +116,8 @@ typedef struct {
  *   k_pool         dev  [n_pages][Hkv][Bt][d] kv_dtype
  *   n_pages             number of pages in k_pool (> 0)
  *   block_to_page  dev  int32, read at [first_block, first_block + n_blocks)
- *   index          dev  float [>= first_block + n_blocks][Hkv][d]
+ *   index          dev  float, one layer in the tiled layout, at least
+ *                       kvmem_index_bytes(geom, first_block + n_blocks) bytes
  *   stream              hipStream_t
  * n_blocks == 0 is a no-op.  A page id outside [0, n_pages) yields a NaN row. */
 kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
@@ -145,7 +154,8 @@ size_t kvmem_select_workspace_bytes(const kvmem_geom *geom, int32_t n_layers, in
  *   view_pages[s][i] = block_to_page[view_blocks[s][i]]
  *
  *   q              dev  float [n_layers][n_q][Hq][d]
- *   index          dev  float [n_layers][M][Hkv][d]
+ *   index          dev  float, n_layers consecutive layers in the tiled
+ *                       layout, each kvmem_index_bytes(geom, M) bytes
  *   n_blocks            M; requires n_sink + n_recent < M and |C| <= 65536
  *   model_ctx_tokens, gpu_kv_tokens   B_model and B_gpu of Eq. 5
  *   mode                kvmem_reduce

@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
             acc += sm_o[w][r][d] * f;
             l += sm_l[w][r] * f;
         }
-        float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r) * (D + 2);
+        float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r) * (D + kPartStride);
         dst[d] = any_bad ? __builtin_nanf("") : acc;
         if (d == 0) {
             dst[D] = mx;
@@ -182,26 +182,301 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
     }
 }
 
+// Fast path for 16-lane token rows (bf16 with d = 128, or f32 with d = 64) and
+// RH >= 4 query rows per KV head.  Work goes in units of 16 tokens of a page:
+// lane group lg (a 16-lane DPP row) takes tokens 4i + lg, i < 4.  The 4*RH
+// partial logits of a lane are summed over its row with row_transpose_reduce16,
+// after which lane lp owns query row r = lp % RH for RH/4 token slots; it alone
+// exponentiates those scores, keeps the running max and sum of its row, and
+// the probabilities reach the other 15 lanes through row_newbcast.  Rescaling
+// of the accumulators is skipped unless some running max grew.  The next
+// unit's K and V are loaded while the current one is processed.
+template <typename T, int D, int BT, int RH>
+__global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
+    const float *__restrict__ q, const T *__restrict__ k_pool, const T *__restrict__ v_pool,
+    int64_t n_pages, const int32_t *__restrict__ view_pages, int n_sel, int n_view,
+    int last_page_tokens, int n_kv_heads, int n_q_heads, int group, int rows_total,
+    int pages_per_split, int n_splits, float qscale, float *__restrict__ part) {
+    constexpr int VEC = Vec16<T>::N;
+    static_assert(D / VEC == 16, "one token row per 16-lane DPP row");
+    static_assert(RH >= 4 && RH <= 16 && BT % 16 == 0, "shape of the fast path");
+    constexpr int NV = 4 * RH;         // partial logits per lane per unit
+    constexpr int NC = NV / 16;        // finished logits per lane per unit
+    constexpr int UNITS = BT / 16;     // 16-token units per page
+    __shared__ float sm_o[kAttnWaves][RH][D];
+    __shared__ float sm_m[kAttnWaves][RH], sm_l[kAttnWaves][RH];
+    __shared__ int sm_bad[kAttnWaves];
+
+    const int split = blockIdx.x, g = blockIdx.y, row0 = blockIdx.z * RH;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int lg = lane / 16, lp = lane % 16;
+    const int my_r = lp % RH;
+    const int32_t *vpages = view_pages + (int64_t)(n_sel == 1 ? 0 : g) * n_view;
+    const int p_begin = split * pages_per_split;
+    const int p_end = min(n_view, p_begin + pages_per_split);
+
+    float qr[RH][VEC];
+#pragma unroll
+    for (int r = 0; r < RH; ++r) {
+        const int row = row0 + r, m = row / group, hh = row % group;
+        const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D + lp * VEC;
+#pragma unroll
+        for (int e = 0; e < VEC; e += 4) {
+            const float4 v = *reinterpret_cast<const float4 *>(qp + e);
+            qr[r][e] = v.x * qscale; qr[r][e + 1] = v.y * qscale;
+            qr[r][e + 2] = v.z * qscale; qr[r][e + 3] = v.w * qscale;
+        }
+    }
+    float o[RH][VEC];
+#pragma unroll
+    for (int r = 0; r < RH; ++r)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[r][e] = 0.f;
+    float m_own = -INFINITY, l_own = 0.f;
+    int bad = 0;
+
+    // unit u of this wave: page p_begin + wave + 4*(u / UNITS), tokens 16*(u % UNITS) ...
+    const int n_my_pages = p_end - p_begin - wave > 0 ? (p_end - p_begin - wave + kAttnWaves - 1) / kAttnWaves : 0;
+    const int n_units = n_my_pages * UNITS;
+    auto fetch = [&](int u, uint4 (&kr)[4], uint4 (&vr)[4], int &ntok_out) {
+        const int pi = p_begin + wave + kAttnWaves * (u / UNITS);
+        const int t0 = 16 * (u % UNITS);
+        const int64_t page = vpages[pi];
+        const bool ok = page >= 0 && page < n_pages;
+        bad |= ok ? 0 : 1;
+        const int ntok = ok ? (pi == n_view - 1 ? last_page_tokens : BT) - t0 : 0;
+        ntok_out = ntok;
+        const int64_t off = ((ok ? page : 0) * n_kv_heads + g) * (int64_t)BT * D + (int64_t)t0 * D + lp * VEC;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int t = 4 * i + lg;
+            if (t < ntok) {
+                kr[i] = *reinterpret_cast<const uint4 *>(k_pool + off + (int64_t)t * D);
+                vr[i] = *reinterpret_cast<const uint4 *>(v_pool + off + (int64_t)t * D);
+            } else {
+                kr[i] = make_uint4(0u, 0u, 0u, 0u);
+                vr[i] = make_uint4(0u, 0u, 0u, 0u);
+            }
+        }
+    };
+    auto widen = [](const uint4 &w, float (&out)[VEC]) {
+        if constexpr (VEC == 8) {
+            const uint32_t x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                out[2 * i] = __uint_as_float(x[i] << 16);
+                out[2 * i + 1] = __uint_as_float(x[i] & 0xffff0000u);
+            }
+        } else {
+            out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+            out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
+        }
+    };
+    auto process = [&](const uint4 (&kr)[4], const uint4 (&vr)[4], int ntok) {
+        // partial logits: value v = i*RH + r
+        float part[NV];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float kx[VEC];
+            widen(kr[i], kx);
+#pragma unroll
+            for (int r = 0; r < RH; ++r) {
+                float acc = 0.f;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc += qr[r][e] * kx[e];
+                part[i * RH + r] = acc;
+            }
+        }
+        // finished logits: slot c holds value c*16 + lp, i.e. token slot
+        // (c*16 + lp) / RH of row my_r
+        float sc[NC];
+        float pm = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            float chunk[16];
+#pragma unroll
+            for (int k = 0; k < 16; ++k) chunk[k] = part[c * 16 + k];
+            const float sv = row_transpose_reduce16(chunk, lp);
+            const int t = 4 * ((c * 16 + lp) / RH) + lg;
+            sc[c] = t < ntok ? sv : -INFINITY;
+            pm = fmaxf(pm, sc[c]);
+        }
+        // row maximum over the lanes that share my_r
+        if constexpr (RH < 16) pm = fmaxf(pm, dpp_f<dpp_row_ror(RH)>(pm));
+        if constexpr (RH < 8) pm = fmaxf(pm, dpp_f<dpp_row_ror(2 * RH)>(pm));
+        if constexpr (RH < 4) pm = fmaxf(pm, dpp_f<dpp_row_ror(4 * RH)>(pm));
+        const float mn = fmaxf(m_own, pm);
+        const float msafe = mn == -INFINITY ? 0.f : mn;
+        if (__any(mn > m_own)) {
+            const float alpha = exp2f(m_own - msafe);  // 0 while m_own is -inf
+            l_own *= alpha;
+            float al[RH];
+            static_for<RH>([&](auto r) { al[r] = dpp_f<dpp_row_bcast(r)>(alpha); });
+#pragma unroll
+            for (int r = 0; r < RH; ++r)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) o[r][e] *= al[r];
+        }
+        m_own = mn;
+        float pc[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            pc[c] = exp2f(sc[c] - msafe);
+            l_own += pc[c];
+        }
+        // p for every (token slot i, row r): value i*RH + r lives in lane
+        // (i*RH + r) % 16, slot (i*RH + r) / 16
+        static_for<4>([&](auto i) {
+            float vx[VEC];
+            widen(vr[i], vx);
+            static_for<RH>([&](auto r) {
+                constexpr int v = i * RH + r;
+                const float p = dpp_f<dpp_row_bcast(v % 16)>(pc[v / 16]);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) o[r][e] += p * vx[e];
+            });
+        });
+    };
+
+    // two statically named buffers: unit u+1 loads while unit u is processed
+    uint4 ka[4], va[4], kb[4], vb[4];
+    int na = 0, nb = 0;
+    if (n_units > 0) fetch(0, ka, va, na);
+    for (int u = 0; u < n_units; u += 2) {
+        if (u + 1 < n_units) fetch(u + 1, kb, vb, nb);
+        process(ka, va, na);
+        if (u + 1 >= n_units) break;
+        if (u + 2 < n_units) fetch(u + 2, ka, va, na);
+        process(kb, vb, nb);
+    }
+
+    // per lane group: row sums over the lanes sharing a row, then broadcast
+    float lsum = l_own;
+    if constexpr (RH < 16) lsum += dpp_f<dpp_row_ror(RH)>(lsum);
+    if constexpr (RH < 8) lsum += dpp_f<dpp_row_ror(2 * RH)>(lsum);
+    float mrow[RH], lrow[RH];
+    static_for<RH>([&](auto r) {
+        mrow[r] = dpp_f<dpp_row_bcast(r)>(m_own);
+        lrow[r] = dpp_f<dpp_row_bcast(r)>(lsum);
+    });
+    // merge the 4 lane groups of the wave (lanes lp, lp+16, lp+32, lp+48)
+#pragma unroll
+    for (int r = 0; r < RH; ++r) {
+        float mx = mrow[r];
+        mx = fmaxf(mx, shfl_xor_f(mx, 16));
+        mx = fmaxf(mx, shfl_xor_f(mx, 32));
+        const float f = mrow[r] == -INFINITY ? 0.f : exp2f(mrow[r] - mx);
+        float l = lrow[r] * f;
+        l += shfl_xor_f(l, 16);
+        l += shfl_xor_f(l, 32);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float x = o[r][e] * f;
+            x += shfl_xor_f(x, 16);
+            x += shfl_xor_f(x, 32);
+            o[r][e] = x;
+        }
+        if (lg == 0) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) sm_o[wave][r][lp * VEC + e] = o[r][e];
+        }
+        if (lane == 0) {
+            sm_m[wave][r] = mx;
+            sm_l[wave][r] = l;
+        }
+    }
+    if (lane == 0) sm_bad[wave] = 0;
+    __syncthreads();
+    if (bad) atomicOr(&sm_bad[wave], 1);
+    __syncthreads();
+    const bool any_bad = sm_bad[0] | sm_bad[1] | sm_bad[2] | sm_bad[3];
+    for (int idx = threadIdx.x; idx < RH * D; idx += kAttnThreads) {
+        const int r = idx / D, d = idx % D;
+        float mx = sm_m[0][r];
+#pragma unroll
+        for (int w = 1; w < kAttnWaves; ++w) mx = fmaxf(mx, sm_m[w][r]);
+        float acc = 0.f, l = 0.f;
+#pragma unroll
+        for (int w = 0; w < kAttnWaves; ++w) {
+            const float f = sm_m[w][r] == -INFINITY ? 0.f : exp2f(sm_m[w][r] - mx);
+            acc += sm_o[w][r][d] * f;
+            l += sm_l[w][r] * f;
+        }
+        float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r) * (D + kPartStride);
+        dst[d] = any_bad ? __builtin_nanf("") : acc;
+        if (d == 0) {
+            dst[D] = mx;
+            dst[D + 1] = l;
+        }
+    }
+}
+
+constexpr int kCombineThreads = 256;
+
+// One workgroup per (KV head, row).  The split weights 2^(m_s - M) are formed
+// once into LDS; then D/4 lanes read one split's partial row as float4s and the
+// workgroup walks kCombineThreads/(D/4) splits at a time, so every thread keeps
+// many independent loads in flight.
 template <int D>
-__global__ __launch_bounds__(D) void attn_combine_kernel(const float *__restrict__ part, int n_splits,
-                                                         int rows_total, int n_q_heads, int group,
-                                                         float *__restrict__ out,
-                                                         float *__restrict__ lse) {
-    const int g = blockIdx.x / rows_total, r = blockIdx.x % rows_total, d = threadIdx.x;
-    const int64_t stride = (int64_t)rows_total * (D + 2);
-    const float *pr = part + ((int64_t)g * n_splits * rows_total + r) * (D + 2);
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
+    const float *__restrict__ part, int n_splits, int rows_total, int n_q_heads, int group,
+    float *__restrict__ out, float *__restrict__ lse) {
+    constexpr int LPS = D / 4;                     // lanes per split row
+    constexpr int SPI = kCombineThreads / LPS;     // splits per iteration
+    extern __shared__ float sm_w[];                // [n_splits] weights
+    __shared__ float sm_red[kCombineThreads / kWave];
+    __shared__ float4 sm_acc[SPI][LPS];
+    const int g = blockIdx.x / rows_total, r = blockIdx.x % rows_total;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int64_t stride = (int64_t)rows_total * (D + kPartStride);
+    const float *pr = part + ((int64_t)g * n_splits * rows_total + r) * (D + kPartStride);
+
     float mx = -INFINITY;
-    for (int s = 0; s < n_splits; ++s) mx = fmaxf(mx, pr[s * stride + D]);
-    float acc = 0.f, l = 0.f;
-    for (int s = 0; s < n_splits; ++s) {
+    for (int s = tid; s < n_splits; s += kCombineThreads) mx = fmaxf(mx, pr[s * stride + D]);
+    mx = wave_max(mx);
+    if (lane == 0) sm_red[wave] = mx;
+    __syncthreads();
+    mx = sm_red[0];
+#pragma unroll
+    for (int w = 1; w < kCombineThreads / kWave; ++w) mx = fmaxf(mx, sm_red[w]);
+    __syncthreads();
+    float l = 0.f;
+    for (int s = tid; s < n_splits; s += kCombineThreads) {
         const float ms = pr[s * stride + D];
         const float f = ms == -INFINITY ? 0.f : exp2f(ms - mx);
-        acc += pr[s * stride + d] * f;
+        sm_w[s] = f;
         l += pr[s * stride + D + 1] * f;
     }
-    const int m = r / group, h = (blockIdx.x / rows_total) * group + r % group;
-    out[((int64_t)m * n_q_heads + h) * D + d] = acc / l;
-    if (lse && d == 0) lse[(int64_t)m * n_q_heads + h] = (mx + log2f(l)) * kLn2;
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) l += shfl_xor_f(l, o);
+    if (lane == 0) sm_red[wave] = l;
+    __syncthreads();
+    l = 0.f;
+#pragma unroll
+    for (int w = 0; w < kCombineThreads / kWave; ++w) l += sm_red[w];
+
+    const int sl = tid / LPS, dq = tid % LPS;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int s = sl; s < n_splits; s += SPI) {
+        const float4 v = *reinterpret_cast<const float4 *>(pr + s * stride + dq * 4);
+        const float f = sm_w[s];
+        acc.x += v.x * f; acc.y += v.y * f; acc.z += v.z * f; acc.w += v.w * f;
+    }
+    sm_acc[sl][dq] = acc;
+    __syncthreads();
+    if (tid < LPS) {
+        float4 t = sm_acc[0][tid];
+        for (int i = 1; i < SPI; ++i) {
+            const float4 u = sm_acc[i][tid];
+            t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
+        }
+        const float inv = 1.f / l;
+        const int m = r / group, h = g * group + r % group;
+        *reinterpret_cast<float4 *>(out + ((int64_t)m * n_q_heads + h) * D + tid * 4) =
+            make_float4(t.x * inv, t.y * inv, t.z * inv, t.w * inv);
+        if (lse && tid == 0) lse[(int64_t)m * n_q_heads + h] = (mx + log2f(l)) * kLn2;
+    }
 }
 
 template <typename T, int D, int BT, int RH>
@@ -216,10 +491,26 @@ hipError_t launch_rh(const AttnPlan &p, const float *q, const void *k_pool, cons
     return hipGetLastError();
 }
 
+template <typename T, int D, int BT, int RH>
+hipError_t launch_row16(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
+                        int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
+                        hipStream_t stream) {
+    dim3 grid(p.n_splits, p.n_kv_heads, p.rows_per_head / RH);
+    hipLaunchKernelGGL((attn_splitk_row16_kernel<T, D, BT, RH>), grid, dim3(kAttnThreads), 0, stream, q,
+                       static_cast<const T *>(k_pool), static_cast<const T *>(v_pool), n_pages,
+                       view_pages, p.n_sel, p.n_view, p.last_page_tokens, p.n_kv_heads, p.n_q_heads,
+                       p.group, p.rows_per_head, p.pages_per_split, p.n_splits, qscale, part);
+    return hipGetLastError();
+}
+
 template <typename T, int D, int BT>
 hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const void *v, int64_t n_pages,
                      const int32_t *vp, float qscale, float *part, hipStream_t stream) {
     const int rows = p.rows_per_head;
+    if constexpr (D / Vec16<T>::N == 16) {
+        if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        if (rows % 4 == 0) return launch_row16<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
+    }
     if (rows % 8 == 0) return launch_rh<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
     if (rows % 4 == 0) return launch_rh<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
     if (rows % 2 == 0) return launch_rh<T, D, BT, 2>(p, q, k, v, n_pages, vp, qscale, part, stream);
@@ -254,12 +545,13 @@ hipError_t launch_sparse_attn(const AttnPlan &p, const float *q, const void *k_p
                  : launch_d<float, 64>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
     if (e != hipSuccess) return e;
     const dim3 grid(p.n_kv_heads * p.rows_per_head);
+    const size_t lds = sizeof(float) * (size_t)p.n_splits;
     if (p.head_dim == 128)
-        hipLaunchKernelGGL((attn_combine_kernel<128>), grid, dim3(128), 0, stream, part, p.n_splits,
-                           p.rows_per_head, p.n_q_heads, p.group, out, lse);
+        hipLaunchKernelGGL((attn_combine_kernel<128>), grid, dim3(kCombineThreads), lds, stream, part,
+                           p.n_splits, p.rows_per_head, p.n_q_heads, p.group, out, lse);
     else
-        hipLaunchKernelGGL((attn_combine_kernel<64>), grid, dim3(64), 0, stream, part, p.n_splits,
-                           p.rows_per_head, p.n_q_heads, p.group, out, lse);
+        hipLaunchKernelGGL((attn_combine_kernel<64>), grid, dim3(kCombineThreads), lds, stream, part,
+                           p.n_splits, p.rows_per_head, p.n_q_heads, p.group, out, lse);
     return hipGetLastError();
 }
 

@@ -1,12 +1,16 @@
-// Mean-K retrieval index (Eq. 9): index[b][g][:] = mean over the Bt keys of
-// block b's page for KV head g.
+// Mean-K retrieval index (Eq. 9): for block b and KV head g, the mean over the
+// Bt keys of page block_to_page[b], written in the tiled index layout
+// (float [ceil(M/64)][Hkv][d/4][64][4]).
 //
-// One wave per (block, KV head).  The page slice [Bt][d] is contiguous, so each
-// lane reads 16 bytes per token row (a row is d*elem bytes; 64/LPR rows per
-// wave instruction) and the loads of a wave cover whole rows.  Sums are kept in
-// fp64, where adding at most 64 bf16 or fp32 values of ordinary range is
-// exact; the result is rounded once to fp32, so it does not depend on the
-// order of summation.
+// One workgroup per (64-block tile, KV head).  Each wave reduces 16 of the
+// tile's blocks: a page slice [Bt][d] is contiguous, so LPR = d*elem/16 lanes
+// read one token row with 16-byte loads and 64/LPR rows go per instruction;
+// four blocks are loaded per step to keep loads in flight.  Sums are kept in
+// fp64: adding Bt <= 64 bf16 values (8-bit significands) or fp32 values whose
+// magnitudes span less than 2^23 is exact there, so the result -- rounded once
+// to fp32 -- does not depend on the order of summation.  The finished means
+// are staged as a [64][d] tile in LDS and written out so that each wave store
+// covers 1 KB of contiguous index.
 #include <math.h>
 
 #include "kvmem_device.h"
@@ -15,50 +19,88 @@
 namespace kvmem {
 namespace {
 
-constexpr int kWavesPerGroup = 4;
+constexpr int kWaves = 4;
+constexpr int kBlocksPerStep = 4;
 
 template <typename T, int D>
-__global__ __launch_bounds__(kWavesPerGroup *kWave) void build_index_kernel(
+__global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ block_to_page,
     int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens,
     float *__restrict__ index) {
     constexpr int VEC = Vec16<T>::N;  // elements per lane per row
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int64_t pair = (int64_t)blockIdx.x * kWavesPerGroup + wave;
-    if (pair >= (int64_t)n_blocks * n_kv_heads) return;  // uniform per wave
-    const int32_t b = first_block + (int32_t)(pair / n_kv_heads);
-    const int g = (int)(pair % n_kv_heads);
-    const int tg = lane / LPR, lp = lane % LPR;
-    const int64_t page = block_to_page[b];
-    const bool ok = page >= 0 && page < n_pages;
+    constexpr int PAD = D + 4;        // LDS row stride (floats): conflict-free column reads
+    __shared__ float tile_buf[kIndexTile * PAD];
 
-    double acc[VEC];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int tg = lane / LPR, lp = lane % LPR;
+    const int g = blockIdx.y;
+    const int64_t tile = first_block / kIndexTile + blockIdx.x;
+    const int64_t b_tile0 = tile * kIndexTile;
+    const int64_t b_lo = b_tile0 > first_block ? b_tile0 : first_block;
+    const int64_t b_end = (int64_t)first_block + n_blocks;
+    const int64_t b_hi = b_tile0 + kIndexTile < b_end ? b_tile0 + kIndexTile : b_end;
+    const double inv = 1.0 / (double)block_tokens;
+
+    // wave w reduces tile slots w, w+4, w+8, ... (kBlocksPerStep at a time)
+    for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * kBlocksPerStep) {
+        double acc[kBlocksPerStep][VEC];
+        bool ok[kBlocksPerStep];
+        const T *base[kBlocksPerStep];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
-    if (ok) {
-        const T *base = k_pool + ((page * n_kv_heads + g) * (int64_t)block_tokens) * D + lp * VEC;
+        for (int k = 0; k < kBlocksPerStep; ++k) {
+            const int64_t b = b_tile0 + s0 + k * kWaves;
+            const bool in = b >= b_lo && b < b_hi;
+            const int64_t page = in ? block_to_page[b] : -1;
+            ok[k] = in && page >= 0 && page < n_pages;
+            base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D + lp * VEC;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[k][e] = 0.0;
+        }
         for (int t = tg; t < block_tokens; t += TG) {
-            float v[VEC];
-            Vec16<T>::load(base + (int64_t)t * D, v);
+            float v[kBlocksPerStep][VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[e] += (double)v[e];
+            for (int k = 0; k < kBlocksPerStep; ++k) {
+                if (ok[k]) {
+                    Vec16<T>::load(base[k] + (int64_t)t * D, v[k]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) v[k][e] = 0.f;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kBlocksPerStep; ++k)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[k][e] += (double)v[k][e];
+        }
+#pragma unroll
+        for (int k = 0; k < kBlocksPerStep; ++k) {
+#pragma unroll
+            for (int o = LPR; o < kWave; o <<= 1)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[k][e] += shfl_xor_d(acc[k][e], o);
+            if (tg == 0) {
+                float *dst = tile_buf + (s0 + k * kWaves) * PAD + lp * VEC;
+#pragma unroll
+                for (int e = 0; e < VEC; e += 4)
+                    *reinterpret_cast<float4 *>(dst + e) = ok[k]
+                        ? make_float4((float)(acc[k][e] * inv), (float)(acc[k][e + 1] * inv),
+                                      (float)(acc[k][e + 2] * inv), (float)(acc[k][e + 3] * inv))
+                        : make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
+                                      __builtin_nanf(""));
+            }
         }
     }
-#pragma unroll
-    for (int o = LPR; o < kWave; o <<= 1)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += shfl_xor_d(acc[e], o);
-    if (tg == 0) {
-        float *dst = index + ((int64_t)b * n_kv_heads + g) * D + lp * VEC;
-        const double inv = 1.0 / (double)block_tokens;
-        float outv[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) outv[e] = ok ? (float)(acc[e] * inv) : __builtin_nanf("");
-#pragma unroll
-        for (int e = 0; e < VEC; e += 4)
-            *reinterpret_cast<float4 *>(dst + e) = make_float4(outv[e], outv[e + 1], outv[e + 2], outv[e + 3]);
+    __syncthreads();
+    // write the tile: for each 4-float column j4, 64 consecutive blocks
+    float *out = index + ((tile * n_kv_heads + g) * (D / 4)) * (kIndexTile * 4);
+    for (int i = threadIdx.x; i < (D / 4) * kIndexTile; i += kWaves * kWave) {
+        const int j4 = i / kIndexTile, slot = i % kIndexTile;
+        const int64_t b = b_tile0 + slot;
+        if (b < b_lo || b >= b_hi) continue;
+        const float4 v = *reinterpret_cast<const float4 *>(tile_buf + slot * PAD + j4 * 4);
+        *reinterpret_cast<float4 *>(out + ((int64_t)j4 * kIndexTile + slot) * 4) = v;
     }
 }
 
@@ -66,11 +108,12 @@ template <typename T, int D>
 hipError_t launch_t(int n_kv_heads, int block_tokens, const void *k_pool, int64_t n_pages,
                     const int32_t *block_to_page, int32_t first_block, int32_t n_blocks,
                     float *index, hipStream_t stream) {
-    const int64_t pairs = (int64_t)n_blocks * n_kv_heads;
-    const int64_t groups = (pairs + kWavesPerGroup - 1) / kWavesPerGroup;
-    hipLaunchKernelGGL((build_index_kernel<T, D>), dim3((unsigned)groups), dim3(kWavesPerGroup * kWave),
-                       0, stream, static_cast<const T *>(k_pool), n_pages, block_to_page,
-                       first_block, n_blocks, n_kv_heads, block_tokens, index);
+    const int64_t t0 = first_block / kIndexTile;
+    const int64_t t1 = ((int64_t)first_block + n_blocks + kIndexTile - 1) / kIndexTile;
+    dim3 grid((unsigned)(t1 - t0), (unsigned)n_kv_heads);
+    hipLaunchKernelGGL((build_index_kernel<T, D>), grid, dim3(kWaves * kWave), 0, stream,
+                       static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
+                       n_kv_heads, block_tokens, index);
     return hipGetLastError();
 }
 

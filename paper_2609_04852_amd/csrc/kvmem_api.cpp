@@ -139,6 +139,8 @@ kvmem_status make_attn_plan(const kvmem_geom *g, int32_t n_q, int32_t n_sel, int
     p.n_view = n_view;
     p.last_page_tokens = last_page_tokens;
     kvmem::plan_attn_layout(p);
+    if (p.n_splits > kvmem::kAttnMaxSplits)
+        return fail(KVMEM_ERR_UNSUPPORTED, "a view of %d pages is longer than this build handles", n_view);
     return KVMEM_OK;
 }
 
@@ -152,6 +154,16 @@ kvmem_status hip_status(hipError_t e, const char *what) {
 extern "C" {
 
 const char *kvmem_last_error(void) { return g_error.c_str(); }
+
+size_t kvmem_index_bytes(const kvmem_geom *geom, int32_t n_blocks) {
+    if (check_geom(geom) != KVMEM_OK) return 0;
+    if (n_blocks < 0) {
+        fail(KVMEM_ERR_SHAPE, "n_blocks %d is negative", n_blocks);
+        return 0;
+    }
+    ok();
+    return sizeof(float) * (size_t)kvmem::index_layer_floats(n_blocks, geom->n_kv_heads, geom->head_dim);
+}
 
 kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
                                const int32_t *block_to_page, int32_t first_block,

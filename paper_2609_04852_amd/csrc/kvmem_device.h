@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace kvmem {
 
 constexpr int kWave = 64;
@@ -39,6 +42,75 @@ struct Vec16<uint16_t> {
 };
 
 __device__ inline float shfl_xor_f(float v, int mask) { return __shfl_xor(v, mask, kWave); }
+
+// DPP lane patterns inside one 16-lane row (gfx9 encodings; row_newbcast is gfx90a+).
+constexpr int kDppRowMirror = 0x140;      // lane i <- lane 15-i
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <- lane 7-i within each half row
+constexpr int kDppQuadXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int dpp_row_ror(int n) { return 0x120 + n; }       // rotate within the row by n
+constexpr int dpp_row_bcast(int n) { return 0x150 + n; }     // lane n of the row to all 16
+
+// Calls f(std::integral_constant<int, i>{}) for i = 0 .. N-1, so that i can be
+// used where a constant expression is needed (DPP controls, array indices).
+template <typename F, int... I>
+__device__ inline void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int CTRL>
+__device__ inline float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum 16 values held by each of the 16 lanes of a DPP row so that lane i ends
+// with the row's total of value i.  Four halving steps pair lane i with its
+// mirror (bit 3), half-mirror (bit 2) and quad neighbours (bits 1, 0): each lane
+// keeps the half of its values selected by that bit and adds the partner's copy
+// of the same half.  15 DPP adds for 16 sums; no LDS traffic.
+__device__ inline float row_transpose_reduce16(const float (&in)[16], int lp) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = in[k];
+    {
+        const bool up = (lp & 8) != 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const float a = v[k] + dpp_f<kDppRowMirror>(v[k]);
+            const float b = v[k + 8] + dpp_f<kDppRowMirror>(v[k + 8]);
+            v[k] = up ? b : a;
+        }
+    }
+    {
+        const bool up = (lp & 4) != 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float a = v[k] + dpp_f<kDppRowHalfMirror>(v[k]);
+            const float b = v[k + 4] + dpp_f<kDppRowHalfMirror>(v[k + 4]);
+            v[k] = up ? b : a;
+        }
+    }
+    {
+        const bool up = (lp & 2) != 0;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const float a = v[k] + dpp_f<kDppQuadXor2>(v[k]);
+            const float b = v[k + 2] + dpp_f<kDppQuadXor2>(v[k + 2]);
+            v[k] = up ? b : a;
+        }
+    }
+    {
+        const bool up = (lp & 1) != 0;
+        const float a = v[0] + dpp_f<kDppQuadXor1>(v[0]);
+        const float b = v[1] + dpp_f<kDppQuadXor1>(v[1]);
+        v[0] = up ? b : a;
+    }
+    return v[0];
+}
 __device__ inline double shfl_xor_d(double v, int mask) { return __shfl_xor(v, mask, kWave); }
 
 // Reduce N partial values held by every lane of a team of W consecutive lanes

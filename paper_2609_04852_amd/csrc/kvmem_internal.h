@@ -11,41 +11,72 @@ namespace kvmem {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// ---- Mean-K index layout -------------------------------------------------
+// The index of one layer is stored in tiles of 64 blocks:
+//   float [ceil(M/64)][Hkv][d/4][64][4]
+// so that, for one KV head and one 4-float slice of the head dimension, the
+// 64 blocks of a tile are 1 KB of contiguous memory: a wave scores 64 blocks
+// with one lane per block and fully coalesced 16-byte loads.
+constexpr int kIndexTile = 64;
+__host__ __device__ inline int64_t index_tiles(int64_t n_blocks) { return (n_blocks + kIndexTile - 1) / kIndexTile; }
+__host__ __device__ inline int64_t index_layer_floats(int64_t n_blocks, int n_kv_heads, int head_dim) {
+    return index_tiles(n_blocks) * kIndexTile * n_kv_heads * head_dim;
+}
+
 // ---- select ------------------------------------------------------------
-// Blocks scored by one workgroup of the logit kernel (at least; see score_tile_for).
-constexpr int kScoreTile = 64;
-// Tile size the logit kernel uses for this shape (a multiple of its step).
-int score_tile_for(int head_dim, int n_kv_heads, int rows_per_head);
-// Largest candidate count the single-workgroup top-k keeps in registers.
-constexpr int kTopkMaxCand = 1024 * 64;
+// Index tiles scored by one workgroup of the logit kernel (one per wave).
+constexpr int kScoreTilesPerGroup = 4;
+// Selection: candidates are handled in chunks of kSelChunk by the multi-workgroup
+// stages; the key histogram has kSelBins bins (bits 30..19 of the score key).
+constexpr int kSelChunk = 1024;
+constexpr int kSelBins = 4096;
+constexpr int kTopkMaxCand = 1024 * 64;  // <= 64 chunks per selection row
 
 struct SelectPlan {
     int n_layers, n_q, n_q_heads, n_kv_heads, head_dim, group, rows_per_head;
     int n_blocks, n_sink, n_recent, n_cand, k_eff, n_view, n_sel, mode;
     int n_rows;   // n_layers * n_q * n_q_heads
-    int score_tile;  // blocks per logit workgroup
-    int n_tiles;     // ceil(n_cand / score_tile)
+    int tile_lo;     // first index tile holding a candidate
+    int n_tiles;     // index tiles holding candidates
+    int n_parts;     // logit workgroups along the candidates = partial stats per row
+    int cand_stride; // row stride of logits and score rows (n_cand rounded up to 64)
+    int n_chunks;    // ceil(n_cand / kSelChunk)
     // byte offsets into the workspace
-    size_t off_logits;  // float  [n_rows][n_cand]
-    size_t off_tmax;    // float  [n_rows][n_tiles]
-    size_t off_tsum;    // double [n_rows][n_tiles]
+    size_t off_logits;  // float  [n_rows][cand_stride]
+    size_t off_tmax;    // float  [n_rows][n_parts]
+    size_t off_tsum;    // double [n_rows][n_parts]
     size_t off_rmax;    // float  [n_rows]
     size_t off_rinvz;   // double [n_rows]
-    size_t off_r32;     // float  [n_sel][n_cand]
+    size_t off_r32;     // float  [n_sel][cand_stride]
+    size_t off_hist;    // uint32 [n_sel][kSelBins]     key histogram
+    size_t off_ctrl;    // uint32 [n_sel][8]            pivot bin, threshold key, tie cut
+    size_t off_above;   // uint32 [n_sel][n_chunks]     keys above the pivot bin per chunk
+    size_t off_segcnt;  // uint32 [n_sel][n_chunks]     pivot-bin keys per chunk
+    size_t off_chunkoff;// uint32 [n_sel][n_chunks]     output offset per chunk
+    size_t off_seg;     // uint2  [n_sel][n_chunks * kSelChunk] pivot-bin (key, candidate)
     size_t total;
 };
 
 inline void plan_select_layout(SelectPlan &p) {
     p.n_rows = p.n_layers * p.n_q * p.n_q_heads;
-    p.score_tile = score_tile_for(p.head_dim, p.n_kv_heads, p.rows_per_head);
-    p.n_tiles = (p.n_cand + p.score_tile - 1) / p.score_tile;
+    p.tile_lo = p.n_sink / kIndexTile;
+    p.n_tiles = (int)index_tiles(p.n_blocks - p.n_recent) - p.tile_lo;
+    p.n_parts = (p.n_tiles + kScoreTilesPerGroup - 1) / kScoreTilesPerGroup;
+    p.cand_stride = (p.n_cand + 63) / 64 * 64;
+    p.n_chunks = (p.n_cand + kSelChunk - 1) / kSelChunk;
     size_t o = 0;
-    p.off_logits = o; o = align_up(o + sizeof(float) * (size_t)p.n_rows * p.n_cand);
-    p.off_tmax = o;   o = align_up(o + sizeof(float) * (size_t)p.n_rows * p.n_tiles);
-    p.off_tsum = o;   o = align_up(o + sizeof(double) * (size_t)p.n_rows * p.n_tiles);
+    p.off_logits = o; o = align_up(o + sizeof(float) * (size_t)p.n_rows * p.cand_stride);
+    p.off_tmax = o;   o = align_up(o + sizeof(float) * (size_t)p.n_rows * p.n_parts);
+    p.off_tsum = o;   o = align_up(o + sizeof(double) * (size_t)p.n_rows * p.n_parts);
     p.off_rmax = o;   o = align_up(o + sizeof(float) * (size_t)p.n_rows);
     p.off_rinvz = o;  o = align_up(o + sizeof(double) * (size_t)p.n_rows);
-    p.off_r32 = o;    o = align_up(o + sizeof(float) * (size_t)p.n_sel * p.n_cand);
+    p.off_r32 = o;    o = align_up(o + sizeof(float) * (size_t)p.n_sel * p.cand_stride);
+    p.off_hist = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * kSelBins);
+    p.off_ctrl = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * 8);
+    p.off_above = o;  o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
+    p.off_segcnt = o; o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
+    p.off_chunkoff = o; o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
+    p.off_seg = o;    o = align_up(o + 8 * (size_t)p.n_sel * p.n_chunks * kSelChunk);
     p.total = o;
 }
 
@@ -53,12 +84,14 @@ inline void plan_select_layout(SelectPlan &p) {
 constexpr int kAttnTargetGroups = 2048;  // workgroups the split-K launch aims for
 constexpr int kAttnMinPages = 4;         // pages per split, lower bound
 constexpr int kAttnMaxPages = 64;        // pages per split, upper bound
+constexpr int kAttnMaxSplits = 16384;    // split weights the merge keeps in LDS
+constexpr int kPartStride = 4;           // floats after the D outputs of a partial row: m, l, pad
 
 struct AttnPlan {
     int n_kv_heads, n_q_heads, group, n_q, rows_per_head, head_dim, block_tokens, kv_dtype;
     int n_sel, n_view, last_page_tokens;
     int pages_per_split, n_splits;
-    size_t off_part;  // float [Hkv][n_splits][rows_per_head][head_dim + 2]
+    size_t off_part;  // float [Hkv][n_splits][rows_per_head][head_dim + kPartStride]
     size_t total;
 };
 
@@ -69,7 +102,7 @@ inline void plan_attn_layout(AttnPlan &p) {
     p.n_splits = (p.n_view + pps - 1) / pps;
     p.off_part = 0;
     p.total = align_up(sizeof(float) * (size_t)p.n_kv_heads * p.n_splits * p.rows_per_head *
-                       (p.head_dim + 2));
+                       (p.head_dim + kPartStride));
 }
 
 // ---- launchers (return the launch status) -------------------------------
@@ -77,6 +110,9 @@ hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int bl
                               const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                               int32_t first_block, int32_t n_blocks, float *index,
                               hipStream_t stream);
+
+hipError_t launch_topk(const SelectPlan &p, const int32_t *block_to_page, int32_t *view_blocks,
+                       int32_t *view_pages, char *workspace, hipStream_t stream);
 
 hipError_t launch_select(const SelectPlan &p, const float *q, const float *index, float scale,
                          const int32_t *block_to_page, int32_t *view_blocks, int32_t *view_pages,

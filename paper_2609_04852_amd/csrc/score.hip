@@ -1,21 +1,21 @@
 // Query-conditioned block scoring (Eq. 10).
 //
-//   score_logits  streams the candidate rows of the Mean-K index once.  A team
-//                 of d/4 lanes owns one KV head; every lane holds 16 bytes of
-//                 each index row and the matching slice of the group's query
-//                 rows in registers.  NBK blocks are processed per step and the
-//                 NBK * rows partial dot products are summed across the team
-//                 with a transposing butterfly, so each lane ends with one
-//                 finished logit.  Logits go to the workspace, and every
-//                 workgroup also leaves a (max, sum of exp) pair per query row
-//                 for its tile of blocks.
+//   score_logits  streams the candidate tiles of the Mean-K index once.  The
+//                 tiled layout puts 64 consecutive blocks of one KV head and one
+//                 4-float slice of d in 1 KB, so a wave gives one block to each
+//                 lane, reads with fully coalesced 16-byte loads, and every lane
+//                 finishes its own dot products with the head's G * n_q query
+//                 rows -- no cross-lane sums.  Logits go to the workspace, and
+//                 every workgroup also leaves a (max, sum of exp) pair per query
+//                 row for its four tiles.
 //   score_stats   merges the tile pairs of one query row into the row's global
 //                 softmax normalizer (max, 1/Z), so the tiled result equals the
 //                 softmax over the full candidate set (Sec. 5.2 notes the same
 //                 property for host-staged tiles).
 //   score_reduce  turns logits into probabilities and combines them per block:
 //                 the mean over layers and heads summed over query tokens
-//                 (Eq. 10), or the per-(layer, KV head) maximum.
+//                 (Eq. 10), or the per-(layer, KV head) maximum, and builds the
+//                 score-key histogram the selection stages start from.
 #include <math.h>
 
 #include "kvmem_device.h"
@@ -26,132 +26,100 @@ namespace {
 
 constexpr int kScoreThreads = 256;
 
-template <int D, int RH>
-struct ScoreShape {
-    static constexpr int TEAM = D / 4;                       // lanes per index row
-    static constexpr int TEAMS = kScoreThreads / TEAM;       // teams per workgroup
-    static constexpr int NBK = (TEAM / RH) < 8 ? (TEAM / RH) : 8;  // blocks per step
-    static constexpr int N = NBK * RH;                       // partial sums per lane per step
-    static constexpr int SHIFT = __builtin_ctz(TEAM / N);    // lanes per finished value = 1<<SHIFT
-};
-
+// One wave per (index tile of 64 blocks, KV head): lane i owns block
+// 64*tile + i and accumulates its full dot products with the RH query rows of
+// the head.  For every 4-float slice of the head dimension the wave reads 1 KB
+// of contiguous index; the query values are the same for the whole wave.
 template <int D, int RH>
 __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
     const float *__restrict__ q, const float *__restrict__ index, int n_blocks, int n_kv_heads,
-    int n_q_heads, int group, int n_q, int n_sink, int n_cand, int tile, int n_tiles,
-    int heads_per_wg, float scale, float *__restrict__ logits, float *__restrict__ tmax,
+    int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
+    int n_tiles, int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
     double *__restrict__ tsum) {
-    using S = ScoreShape<D, RH>;
-    constexpr int TEAM = S::TEAM, TEAMS = S::TEAMS, NBK = S::NBK, N = S::N;
-    __shared__ float sm_m[kScoreThreads];
-    __shared__ double sm_s[kScoreThreads];
+    constexpr int NW = kScoreThreads / kWave;
+    __shared__ float sm_m[NW][RH];
+    __shared__ double sm_s[NW][RH];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int g = blockIdx.y, l = blockIdx.z;
+    const int tile = tile_lo + blockIdx.x * NW + wave;
+    const int64_t b = (int64_t)tile * kIndexTile + lane;
+    const int64_t c = b - n_sink;
+    const bool valid = blockIdx.x * NW + wave < n_tiles && c >= 0 && c < n_cand;
 
-    const int team = threadIdx.x / TEAM, lt = threadIdx.x % TEAM;
-    const int bls = TEAMS / heads_per_wg;  // teams sharing one head
-    const int hw = team % heads_per_wg, bl = team / heads_per_wg;
-    const int g = blockIdx.y * heads_per_wg + hw;
-    const int l = blockIdx.z;
-    const int c0 = blockIdx.x * tile;
+    int64_t qrow[RH];
+#pragma unroll
+    for (int r = 0; r < RH; ++r)
+        qrow[r] = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
 
-    // this lane's slice of the group's query rows, r = m * G + hh
-    float qr[RH][4];
+    float acc[RH];
+#pragma unroll
+    for (int r = 0; r < RH; ++r) acc[r] = 0.f;
+    if (blockIdx.x * NW + wave < n_tiles) {
+        const int64_t tiles_per_layer = index_tiles(n_blocks);
+        const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
+                                       (int64_t)(D / 4) * (kIndexTile * 4) + lane * 4;
+#pragma unroll 8
+        for (int j4 = 0; j4 < D / 4; ++j4) {
+            const float4 x = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
+#pragma unroll
+            for (int r = 0; r < RH; ++r) {
+                const float4 qv = *reinterpret_cast<const float4 *>(q + qrow[r] * D + j4 * 4);
+                acc[r] += qv.x * x.x + qv.y * x.y + qv.z * x.z + qv.w * x.w;
+            }
+        }
+    }
+    // logits of this tile (rows contiguous over candidates), and per-wave stats
 #pragma unroll
     for (int r = 0; r < RH; ++r) {
-        const int m = r / group, hh = r % group;
-        const int64_t row = ((int64_t)l * n_q + m) * n_q_heads + g * group + hh;
-        const float4 v = *reinterpret_cast<const float4 *>(q + row * D + lt * 4);
-        qr[r][0] = v.x * scale; qr[r][1] = v.y * scale; qr[r][2] = v.z * scale; qr[r][3] = v.w * scale;
-    }
-    // after the team reduction this lane holds value v = row slot * NBK + block slot
-    const int v = lt >> S::SHIFT;
-    const bool writer = (lt & ((1 << S::SHIFT) - 1)) == 0;
-    const int vr = v / NBK, vk = v % NBK;
-    const int64_t my_row = ((int64_t)l * n_q + vr / group) * n_q_heads + g * group + vr % group;
-
-    const float *ibase = index + (((int64_t)l * n_blocks + n_sink) * n_kv_heads + g) * D + lt * 4;
-    const int64_t row_stride = (int64_t)n_kv_heads * D;
-    float run_m = -INFINITY;
-    double run_s = 0.0;
-    const int steps = tile / (NBK * bls);
-    for (int it = 0; it < steps; ++it) {
-        const int cb = c0 + (it * bls + bl) * NBK;
-        float kv[NBK][4];
-#pragma unroll
-        for (int k = 0; k < NBK; ++k) {
-            const int c = cb + k;
-            if (c < n_cand) {
-                const float4 x = *reinterpret_cast<const float4 *>(ibase + (int64_t)c * row_stride);
-                kv[k][0] = x.x; kv[k][1] = x.y; kv[k][2] = x.z; kv[k][3] = x.w;
-            } else {
-                kv[k][0] = kv[k][1] = kv[k][2] = kv[k][3] = 0.f;
-            }
-        }
-        float part[N];
-#pragma unroll
-        for (int r = 0; r < RH; ++r)
-#pragma unroll
-            for (int k = 0; k < NBK; ++k)
-                part[r * NBK + k] = qr[r][0] * kv[k][0] + qr[r][1] * kv[k][1] +
-                                    qr[r][2] * kv[k][2] + qr[r][3] * kv[k][3];
-        const float s = team_transpose_reduce<N, TEAM>(part, lt);
-        const int c = cb + vk;
-        if (c < n_cand) {
-            if (writer) logits[my_row * n_cand + c] = s;
-            // running (max, sum exp) with one exponential per value
-            const float dlt = s - run_m;
-            const double e = (double)expf(-fabsf(dlt));
-            if (dlt > 0.f) {
-                run_s = run_s * e + 1.0;
-                run_m = s;
-            } else {
-                run_s += e;
-            }
+        const float s = acc[r] * scale;
+        if (valid) logits[qrow[r] * cand_stride + c] = s;
+        float mx = wave_max(valid ? s : -INFINITY);
+        double e = (valid && mx != -INFINITY) ? (double)expf(s - mx) : 0.0;
+        e = wave_sum_d(e);
+        if (lane == 0) {
+            sm_m[wave][r] = mx;
+            sm_s[wave][r] = e;
         }
     }
-    sm_m[threadIdx.x] = writer ? run_m : -INFINITY;
-    sm_s[threadIdx.x] = writer ? run_s : 0.0;
     __syncthreads();
-    // merge the lanes and teams that hold the same (head, row slot)
-    if ((int)threadIdx.x < heads_per_wg * RH) {
-        const int h2 = threadIdx.x / RH, r = threadIdx.x % RH;
-        float mx = -INFINITY;
-        for (int b2 = 0; b2 < bls; ++b2)
-            for (int k = 0; k < NBK; ++k) {
-                const int idx = (b2 * heads_per_wg + h2) * TEAM + ((r * NBK + k) << S::SHIFT);
-                mx = fmaxf(mx, sm_m[idx]);
-            }
+    if ((int)threadIdx.x < RH) {
+        const int r = threadIdx.x;
+        float mx = sm_m[0][r];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) mx = fmaxf(mx, sm_m[w][r]);
         double sum = 0.0;
-        for (int b2 = 0; b2 < bls; ++b2)
-            for (int k = 0; k < NBK; ++k) {
-                const int idx = (b2 * heads_per_wg + h2) * TEAM + ((r * NBK + k) << S::SHIFT);
-                if (sm_m[idx] != -INFINITY) sum += sm_s[idx] * exp((double)sm_m[idx] - (double)mx);
-            }
-        const int g2 = blockIdx.y * heads_per_wg + h2;
-        const int64_t row = ((int64_t)l * n_q + r / group) * n_q_heads + g2 * group + r % group;
-        tmax[row * n_tiles + blockIdx.x] = mx;
-        tsum[row * n_tiles + blockIdx.x] = sum;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            if (sm_m[w][r] != -INFINITY) sum += sm_s[w][r] * exp((double)sm_m[w][r] - (double)mx);
+        tmax[qrow[r] * n_parts + blockIdx.x] = mx;
+        tsum[qrow[r] * n_parts + blockIdx.x] = sum;
     }
 }
 
 __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float *__restrict__ tmax,
                                                                     const double *__restrict__ tsum,
-                                                                    int n_tiles, float *__restrict__ rmax,
-                                                                    double *__restrict__ rinvz) {
+                                                                    int n_parts, float *__restrict__ rmax,
+                                                                    double *__restrict__ rinvz,
+                                                                    uint32_t *__restrict__ hist,
+                                                                    int hist_words) {
+    // the selection histograms are filled by the next kernel; clear them here
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < hist_words; i += kScoreThreads) hist[i] = 0u;
     __shared__ float sm_f[kScoreThreads / kWave];
     __shared__ double sm_d[kScoreThreads / kWave];
     const int row = blockIdx.x;
-    const float *tm = tmax + (int64_t)row * n_tiles;
-    const double *ts = tsum + (int64_t)row * n_tiles;
+    const float *tm = tmax + (int64_t)row * n_parts;
+    const double *ts = tsum + (int64_t)row * n_parts;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     float mx = -INFINITY;
-    for (int i = threadIdx.x; i < n_tiles; i += kScoreThreads) mx = fmaxf(mx, tm[i]);
+    for (int i = threadIdx.x; i < n_parts; i += kScoreThreads) mx = fmaxf(mx, tm[i]);
     mx = wave_max(mx);
     if (lane == 0) sm_f[wave] = mx;
     __syncthreads();
     mx = sm_f[0];
     for (int w = 1; w < kScoreThreads / kWave; ++w) mx = fmaxf(mx, sm_f[w]);
     double z = 0.0;
-    for (int i = threadIdx.x; i < n_tiles; i += kScoreThreads)
+    for (int i = threadIdx.x; i < n_parts; i += kScoreThreads)
         if (tm[i] != -INFINITY) z += ts[i] * exp((double)tm[i] - (double)mx);
     z = wave_sum_d(z);
     if (lane == 0) sm_d[wave] = z;
@@ -164,56 +132,79 @@ __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float 
     }
 }
 
+// Block relevance for one selection row and one chunk of kSelChunk candidates
+// (4 per thread, float4 loads of every contributing logit row):
+//   mean-all:  R_b = (1/(L*Hq)) * sum over every (l, m, h) row of p  (Eq. 10)
+//   group-max: R[l][g][b] = max over the (m, h in g) rows of layer l of p
+// with p = exp(s - max_row) / Z_row summed in fp64.  R is rounded once to fp32.
+// Each workgroup also histograms the selection key (bits(R) + 1) of its
+// candidates by bits 30..19 in LDS and adds the non-empty bins to the row's
+// global histogram, which the selection stages start from.
 __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     const float *__restrict__ logits, const float *__restrict__ rmax,
     const double *__restrict__ rinvz, int n_layers, int n_q, int n_q_heads, int n_kv_heads,
-    int group, int n_blocks, int n_sink, int n_cand, int mode, float *__restrict__ r32,
-    float *__restrict__ scores) {
-    const int n_sel = mode == 0 ? 1 : n_layers * n_kv_heads;
-    for (int64_t b = (int64_t)blockIdx.x * kScoreThreads + threadIdx.x; b < n_blocks;
-         b += (int64_t)gridDim.x * kScoreThreads) {
-        const int64_t c = b - n_sink;
-        if (c < 0 || c >= n_cand) {
-            if (scores)
-                for (int s = 0; s < n_sel; ++s) scores[(int64_t)s * n_blocks + b] = INFINITY;
-            continue;
+    int group, int n_blocks, int n_sink, int n_cand, int64_t cand_stride, int mode,
+    float *__restrict__ r32, float *__restrict__ scores, uint32_t *__restrict__ hist) {
+    __shared__ uint32_t lh[kSelBins];
+    const int sel = blockIdx.y;
+    for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads) lh[i] = 0u;
+    __syncthreads();
+    const int c0 = blockIdx.x * kSelChunk + 4 * threadIdx.x;
+    if (c0 < n_cand) {
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        // mean-all: every (l, m, h) row; group-max: the (m, h in g) rows of layer l
+        const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
+        const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
+#pragma unroll 8
+        for (int i = 0; i < nr; ++i) {
+            const int64_t row = mode == 0 ? (int64_t)i
+                                          : ((int64_t)l * n_q + i / group) * n_q_heads + g * group + i % group;
+            const float4 x = *reinterpret_cast<const float4 *>(logits + row * cand_stride + c0);
+            const float mx = rmax[row];
+            const double iz = rinvz[row];
+            const float xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const double pr = (double)expf(xs[e] - mx) * iz;
+                if (mode == 0) acc[e] += pr;
+                else acc[e] = pr > acc[e] ? pr : acc[e];
+            }
         }
-        if (mode == 0) {
-            // R_b = sum_m mean_{l,h} p_{l,m,h,b}
-            double acc = 0.0;
-            const int n_rows = n_layers * n_q * n_q_heads;
-            for (int row = 0; row < n_rows; ++row)
-                acc += (double)expf(logits[(int64_t)row * n_cand + c] - rmax[row]) * rinvz[row];
-            const float r = (float)(acc / (double)(n_layers * n_q_heads));
-            r32[c] = r;
-            if (scores) scores[b] = r;
-        } else {
-            for (int l = 0; l < n_layers; ++l)
-                for (int g = 0; g < n_kv_heads; ++g) {
-                    double best = 0.0;
-                    for (int m = 0; m < n_q; ++m)
-                        for (int hh = 0; hh < group; ++hh) {
-                            const int64_t row = ((int64_t)l * n_q + m) * n_q_heads + g * group + hh;
-                            const double p = (double)expf(logits[row * n_cand + c] - rmax[row]) * rinvz[row];
-                            best = p > best ? p : best;
-                        }
-                    const int s = l * n_kv_heads + g;
-                    r32[(int64_t)s * n_cand + c] = (float)best;
-                    if (scores) scores[(int64_t)s * n_blocks + b] = (float)best;
-                }
+        float r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            r[e] = mode == 0 ? (float)(acc[e] / (double)(n_layers * n_q_heads)) : (float)acc[e];
+        float *dst = r32 + (int64_t)sel * cand_stride + c0;
+        *reinterpret_cast<float4 *>(dst) = make_float4(r[0], r[1], r[2], r[3]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (c0 + e >= n_cand) continue;
+            const uint32_t key = __float_as_uint(r[e]) + 1u;
+            atomicAdd(&lh[(key >> 19) & (kSelBins - 1)], 1u);
+            if (scores) scores[(int64_t)sel * n_blocks + n_sink + c0 + e] = r[e];
         }
     }
+    if (scores && blockIdx.x == 0) {
+        const int n_res = n_blocks - n_cand;  // sink blocks, then recent blocks
+        for (int i = threadIdx.x; i < n_res; i += kScoreThreads) {
+            const int b = i < n_sink ? i : n_sink + n_cand + (i - n_sink);
+            scores[(int64_t)sel * n_blocks + b] = INFINITY;
+        }
+    }
+    __syncthreads();
+    uint32_t *gh = hist + (int64_t)sel * kSelBins;
+    for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads)
+        if (lh[i]) atomicAdd(&gh[i], lh[i]);
 }
 
 template <int D, int RH>
 hipError_t launch_logits(const SelectPlan &p, const float *q, const float *index, float scale,
                          float *logits, float *tmax, double *tsum, hipStream_t stream) {
-    using S = ScoreShape<D, RH>;
-    const int hpw = p.n_kv_heads < S::TEAMS ? p.n_kv_heads : S::TEAMS;
-    dim3 grid(p.n_tiles, p.n_kv_heads / hpw, p.n_layers);
+    dim3 grid(p.n_parts, p.n_kv_heads, p.n_layers);
     hipLaunchKernelGGL((score_logits_kernel<D, RH>), grid, dim3(kScoreThreads), 0, stream, q, index,
                        p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
-                       p.score_tile, p.n_tiles, hpw, scale, logits, tmax, tsum);
+                       (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
+                       tsum);
     return hipGetLastError();
 }
 
@@ -232,17 +223,6 @@ hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *ind
 
 }  // namespace
 
-int score_tile_for(int head_dim, int n_kv_heads, int rows_per_head) {
-    const int team = head_dim / 4, teams = kScoreThreads / team;
-    const int hpw = n_kv_heads < teams ? n_kv_heads : teams;
-    const int nbk = (team / rows_per_head) < 8 ? (team / rows_per_head) : 8;
-    const int per_step = nbk * (teams / hpw);
-    return per_step > kScoreTile ? per_step : kScoreTile;
-}
-
-hipError_t launch_topk(const SelectPlan &p, const float *r32, const int32_t *block_to_page,
-                       int32_t *view_blocks, int32_t *view_pages, hipStream_t stream);
-
 hipError_t launch_select(const SelectPlan &p, const float *q, const float *index, float scale,
                          const int32_t *block_to_page, int32_t *view_blocks, int32_t *view_pages,
                          float *scores, char *ws, hipStream_t stream) {
@@ -252,20 +232,19 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
     float *rmax = reinterpret_cast<float *>(ws + p.off_rmax);
     double *rinvz = reinterpret_cast<double *>(ws + p.off_rinvz);
     float *r32 = reinterpret_cast<float *>(ws + p.off_r32);
+    uint32_t *hist = reinterpret_cast<uint32_t *>(ws + p.off_hist);
     hipError_t e = p.head_dim == 128
                        ? launch_logits_d<128>(p, q, index, scale, logits, tmax, tsum, stream)
                        : launch_logits_d<64>(p, q, index, scale, logits, tmax, tsum, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(score_stats_kernel, dim3(p.n_rows), dim3(kScoreThreads), 0, stream, tmax, tsum,
-                       p.n_tiles, rmax, rinvz);
+                       p.n_parts, rmax, rinvz, hist, p.n_sel * kSelBins);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    int groups = (p.n_blocks + kScoreThreads - 1) / kScoreThreads;
-    if (groups > 4096) groups = 4096;
-    hipLaunchKernelGGL(score_reduce_kernel, dim3(groups), dim3(kScoreThreads), 0, stream, logits, rmax,
-                       rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group, p.n_blocks,
-                       p.n_sink, p.n_cand, p.mode, r32, scores);
+    hipLaunchKernelGGL(score_reduce_kernel, dim3(p.n_chunks, p.n_sel), dim3(kScoreThreads), 0, stream,
+                       logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
+                       p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return launch_topk(p, r32, block_to_page, view_blocks, view_pages, stream);
+    return launch_topk(p, block_to_page, view_blocks, view_pages, ws, stream);
 }
 
 }  // namespace kvmem

@@ -68,6 +68,8 @@ def lib() -> ctypes.CDLL:
     P, G = ctypes.c_void_p, ctypes.POINTER(kvmem_geom)
     i32, i64, f32, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
     pi32 = ctypes.POINTER(ctypes.c_int32)
+    L.kvmem_index_bytes.argtypes = [G, i32]
+    L.kvmem_index_bytes.restype = sz
     L.kvmem_build_index.argtypes = [G, P, i64, P, i32, i32, P, P]
     L.kvmem_plan_view.argtypes = [G, i32, i32, i32, i64, i64, pi32, pi32]
     L.kvmem_select_workspace_bytes.argtypes = [G, i32, i32, i32, i32, i32, i32]
@@ -123,6 +125,26 @@ def _need(t: torch.Tensor, dtype, name: str):
         raise TypeError(f"{name} must be a contiguous CUDA {dtype} tensor")
 
 
+INDEX_TILE = 64
+
+
+def kvmem_index_bytes(geom: Geom, n_blocks: int) -> int:
+    n = lib().kvmem_index_bytes(ctypes.byref(geom.c()), n_blocks)
+    if n == 0 and n_blocks > 0:
+        raise KvmemError(-2, kvmem_last_error())
+    return n
+
+
+def index_rows(index, n_blocks: int, n_kv_heads: int, head_dim: int):
+    """One layer of the tiled Mean-K index ([T][Hkv][d/4][64][4], torch or
+    numpy) as a [n_blocks][Hkv][d] array (a layout change only)."""
+    t = -(-n_blocks // INDEX_TILE)
+    x = index.reshape(-1)[: t * INDEX_TILE * n_kv_heads * head_dim]
+    x = x.reshape(t, n_kv_heads, head_dim // 4, INDEX_TILE, 4)
+    x = x.permute(0, 3, 1, 2, 4) if isinstance(x, torch.Tensor) else x.transpose(0, 3, 1, 2, 4)
+    return x.reshape(t * INDEX_TILE, n_kv_heads, head_dim)[:n_blocks]
+
+
 def kvmem_build_index(geom: Geom, k_pool: torch.Tensor, block_to_page: torch.Tensor,
                       first_block: int, n_blocks: int, index: torch.Tensor, stream=None):
     _need(block_to_page, torch.int32, "block_to_page")
@@ -131,9 +153,8 @@ def kvmem_build_index(geom: Geom, k_pool: torch.Tensor, block_to_page: torch.Ten
         raise TypeError("k_pool must be a contiguous CUDA tensor")
     if block_to_page.numel() < first_block + n_blocks:
         raise ValueError("block_to_page is shorter than the block range")
-    row = geom.n_kv_heads * geom.head_dim
-    if index.numel() < (first_block + n_blocks) * row:
-        raise ValueError("index is smaller than the block range")
+    if index.numel() * 4 < kvmem_index_bytes(geom, first_block + n_blocks):
+        raise ValueError("index is smaller than the block range needs")
     n_pages = k_pool.numel() // (geom.n_kv_heads * geom.block_tokens * geom.head_dim)
     _check(lib().kvmem_build_index(ctypes.byref(geom.c()), _ptr(k_pool), n_pages,
                                    _ptr(block_to_page), first_block, n_blocks, _ptr(index),
@@ -158,24 +179,22 @@ def kvmem_select_workspace_bytes(geom: Geom, n_layers: int, n_q: int, n_blocks: 
     return n
 
 
-def kvmem_select(geom: Geom, q: torch.Tensor, index: torch.Tensor, n_sink: int, n_recent: int,
-                 model_ctx_tokens: int, gpu_kv_tokens: int, mode: int, scale: float,
+def kvmem_select(geom: Geom, q: torch.Tensor, index: torch.Tensor, n_blocks: int, n_sink: int,
+                 n_recent: int, model_ctx_tokens: int, gpu_kv_tokens: int, mode: int, scale: float,
                  block_to_page: torch.Tensor, view_blocks: torch.Tensor, view_pages: torch.Tensor,
                  workspace: torch.Tensor, scores: torch.Tensor | None = None, stream=None) -> int:
-    """q [L][n_q][Hq][d] float32, index [L][M][Hkv][d] float32.  Returns n_view."""
+    """q [L][n_q][Hq][d] float32; index: L tiled layers (see kvmem_index_bytes).  Returns n_view."""
     _need(q, torch.float32, "q")
     _need(index, torch.float32, "index")
     _need(block_to_page, torch.int32, "block_to_page")
     _need(view_blocks, torch.int32, "view_blocks")
     _need(view_pages, torch.int32, "view_pages")
     _need(workspace, torch.uint8, "workspace")
-    if q.dim() != 4 or index.dim() != 4 or q.shape[0] != index.shape[0]:
-        raise ValueError("q must be [L][n_q][Hq][d] and index [L][M][Hkv][d]")
+    if q.dim() != 4 or tuple(q.shape[2:]) != (geom.n_q_heads, geom.head_dim):
+        raise ValueError("q must be [L][n_q][Hq][d]")
     n_layers, n_q = q.shape[0], q.shape[1]
-    n_blocks = index.shape[1]
-    if tuple(q.shape[2:]) != (geom.n_q_heads, geom.head_dim) or \
-            tuple(index.shape[2:]) != (geom.n_kv_heads, geom.head_dim):
-        raise ValueError("q/index shapes do not match the geometry")
+    if index.numel() * 4 < n_layers * kvmem_index_bytes(geom, n_blocks):
+        raise ValueError("index is smaller than n_layers tiled layers of n_blocks blocks")
     if block_to_page.numel() != n_blocks:
         raise ValueError("block_to_page must have one entry per block")
     k_eff, n_view = kvmem_plan_view(geom, n_blocks, n_sink, n_recent, model_ctx_tokens, gpu_kv_tokens)

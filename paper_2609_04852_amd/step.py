@@ -50,7 +50,7 @@ class LayerState:
         self.block_to_page = torch.from_numpy(np.ascontiguousarray(block_to_page, np.int32)).to(self.device)
         self.n_blocks = int(block_to_page.shape[0])
         g = self.geom
-        self.index = torch.empty((1, self.n_blocks, g.n_kv_heads, g.head_dim), dtype=torch.float32,
+        self.index = torch.empty(K.kvmem_index_bytes(g, self.n_blocks) // 4, dtype=torch.float32,
                                  device=self.device)
         self.k_eff, self.n_view = K.kvmem_plan_view(g, self.n_blocks, self.n_sink, self.n_recent,
                                                     self.budget, self.budget)
@@ -66,6 +66,11 @@ class LayerState:
         self.out = torch.empty((self.n_q, g.n_q_heads, g.head_dim), dtype=torch.float32, device=self.device)
         self.lse = torch.empty((self.n_q, g.n_q_heads), dtype=torch.float32, device=self.device)
 
+    def index_rows(self) -> np.ndarray:
+        """The index as a host [M][Hkv][d] array."""
+        g = self.geom
+        return K.index_rows(self.index.cpu().numpy(), self.n_blocks, g.n_kv_heads, g.head_dim).copy()
+
     def build_index(self, first_block: int = 0, n_blocks: int | None = None, stream=None):
         n = self.n_blocks - first_block if n_blocks is None else n_blocks
         K.kvmem_build_index(self.geom, self.k_pool, self.block_to_page, first_block, n, self.index,
@@ -73,9 +78,9 @@ class LayerState:
 
     def select(self, q: torch.Tensor, with_scores: bool = True, stream=None) -> int:
         """q [1][n_q][Hq][d] (this layer).  Fills view_blocks/view_pages (and scores)."""
-        return K.kvmem_select(self.geom, q, self.index, self.n_sink, self.n_recent, self.budget,
-                              self.budget, self.mode, 0.0, self.block_to_page, self.view_blocks,
-                              self.view_pages, self.select_ws,
+        return K.kvmem_select(self.geom, q, self.index, self.n_blocks, self.n_sink, self.n_recent,
+                              self.budget, self.budget, self.mode, 0.0, self.block_to_page,
+                              self.view_blocks, self.view_pages, self.select_ws,
                               self.scores if with_scores else None, stream)
 
     def attend(self, q: torch.Tensor, view_pages: torch.Tensor | None = None,

@@ -54,7 +54,7 @@ def run_case(cfg, seed, layer=0, budget=None, lpt=None, e2e=True, stats=None):
     st = LayerState(cfg, kp, vp_pool, b2p, budget_tokens=budget)
     st.build_index()
     torch.cuda.synchronize()
-    assert_index_bitwise(st.index[0].cpu().numpy(), index_ref)
+    assert_index_bitwise(st.index_rows(), index_ref)
     log("  gpu: select")
     qd = torch.from_numpy(np.ascontiguousarray(q_l)).cuda()
     n_view = st.select(qd)
@@ -179,7 +179,7 @@ def test_incremental_index_build():
     for lo, hi in [(0, 1000), (1000, 1001), (1001, 4096)]:
         st.build_index(lo, hi - lo)
     torch.cuda.synchronize()
-    assert_index_bitwise(st.index[0].cpu().numpy(), oracle.mean_k(w.k_pool[0], w.block_to_page))
+    assert_index_bitwise(st.index_rows(), oracle.mean_k(w.k_pool[0], w.block_to_page))
 
 
 def test_deterministic():
@@ -234,9 +234,26 @@ def test_out_of_range_pages_give_nan():
     st2 = LayerState(cfg, w.k_pool[0], None, b2p)
     st2.build_index()
     torch.cuda.synchronize()
-    idx = st2.index[0].cpu().numpy()
+    idx = st2.index_rows()
     assert np.isnan(idx[7]).all()
     ok = np.ones(cfg.n_blocks, bool)
     ok[7] = False
     ref = oracle.mean_k(w.k_pool[0], w.block_to_page)
     assert_index_bitwise(idx[ok], ref[ok])
+
+
+def test_all_equal_scores_large():
+    """Every page holds the same keys: all scores tie, the pivot bin holds every
+    candidate (more than the LDS window), and the lowest ids must win."""
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", 20480, 3, 5, 1, W.MEAN_ALL, 7000, planted=0)
+    log("[case] all scores equal, 20472 candidates")
+    w = W.generate(cfg, 14, with_values=False)
+    kp = np.broadcast_to(w.k_pool[0][:1], w.k_pool[0].shape).copy()
+    st = LayerState(cfg, kp, kp, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    vb = st.view_blocks.cpu().numpy()[0]
+    expect = list(range(3)) + list(range(3, 3 + 7000)) + list(range(20480 - 5, 20480))
+    assert vb.tolist() == expect
+    np.testing.assert_array_equal(st.view_pages.cpu().numpy()[0], w.block_to_page[vb])
