@@ -38,7 +38,22 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the CPU-oracle baseline sample (0 disables it)")
     p.add_argument("--graph", action="store_true", help="replay the steps from a captured HIP graph")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run 5 device-to-device copies of MIB MiB (known bytes, for scaling "
+                        "rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
     return p.parse_args()
+
+
+def copy_calibration(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "copies": 5}), flush=True)
 
 
 def source_digest(paths):
@@ -88,6 +103,9 @@ def cpu_oracle_baseline(w, seconds):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): the "
