@@ -190,7 +190,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
 // exponentiates those scores, keeps the running max and sum of its row, and
 // the probabilities reach the other 15 lanes through row_newbcast.  Rescaling
 // of the accumulators is skipped unless some running max grew.  The next
-// unit's K and V are loaded while the current one is processed.
+// unit's K and V are loaded (non-temporal) while the current one is processed.
 template <typename T, int D, int BT, int RH>
 __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     const float *__restrict__ q, const T *__restrict__ k_pool, const T *__restrict__ v_pool,
@@ -251,8 +251,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
         for (int i = 0; i < 4; ++i) {
             const int t = 4 * i + lg;
             if (t < ntok) {
-                kr[i] = *reinterpret_cast<const uint4 *>(k_pool + off + (int64_t)t * D);
-                vr[i] = *reinterpret_cast<const uint4 *>(v_pool + off + (int64_t)t * D);
+                kr[i] = load_stream16(k_pool + off + (int64_t)t * D);
+                vr[i] = load_stream16(v_pool + off + (int64_t)t * D);
             } else {
                 kr[i] = make_uint4(0u, 0u, 0u, 0u);
                 vr[i] = make_uint4(0u, 0u, 0u, 0u);

@@ -13,6 +13,16 @@ constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// 16-byte load of data read exactly once per step (K/V pages, raw keys): the
+// non-temporal hint keeps this stream from evicting what is reused from the
+// caches (the index, logits and tables of the next kernels).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+template <typename T>
+__device__ inline uint4 load_stream16(const T *p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // One 16-byte load of K/V elements widened to fp32.  bf16 values are stored as
 // raw 16-bit patterns; widening is exact.
 template <typename T>
@@ -22,8 +32,9 @@ template <>
 struct Vec16<float> {
     static constexpr int N = 4;
     __device__ static inline void load(const float *p, float (&out)[4]) {
-        float4 v = *reinterpret_cast<const float4 *>(p);
-        out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+        const uint4 v = load_stream16(p);
+        out[0] = __uint_as_float(v.x); out[1] = __uint_as_float(v.y);
+        out[2] = __uint_as_float(v.z); out[3] = __uint_as_float(v.w);
     }
 };
 
@@ -31,7 +42,7 @@ template <>
 struct Vec16<uint16_t> {
     static constexpr int N = 8;
     __device__ static inline void load(const uint16_t *p, float (&out)[8]) {
-        uint4 v = *reinterpret_cast<const uint4 *>(p);
+        const uint4 v = load_stream16(p);
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

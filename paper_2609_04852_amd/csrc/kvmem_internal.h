@@ -26,10 +26,13 @@ __host__ __device__ inline int64_t index_layer_floats(int64_t n_blocks, int n_kv
 // ---- select ------------------------------------------------------------
 // Index tiles scored by one workgroup of the logit kernel (one per wave).
 constexpr int kScoreTilesPerGroup = 4;
-// Selection: candidates are handled in chunks of kSelChunk by the multi-workgroup
-// stages; the key histogram has kSelBins bins (bits 30..19 of the score key).
+// Selection: candidates are handled in chunks of kSelChunk (one workgroup
+// each); the key histogram has kSelBins bins (bits 30..19 of the score key),
+// the second level inside the pivot bin kSelBins2 (bits 18..8).
 constexpr int kSelChunk = 1024;
 constexpr int kSelBins = 4096;
+constexpr int kSelBins2 = 2048;
+constexpr int kSelHistWords = kSelBins + kSelBins2 + 1;  // per selection row, with the pivot-bin count
 constexpr int kTopkMaxCand = 1024 * 64;  // <= 64 chunks per selection row
 
 struct SelectPlan {
@@ -48,12 +51,12 @@ struct SelectPlan {
     size_t off_rmax;    // float  [n_rows]
     size_t off_rinvz;   // double [n_rows]
     size_t off_r32;     // float  [n_sel][cand_stride]
-    size_t off_hist;    // uint32 [n_sel][kSelBins]     key histogram
-    size_t off_ctrl;    // uint32 [n_sel][8]            pivot bin, threshold key, tie cut
+    // uint32 [n_sel][kSelBins] key histogram, [n_sel][kSelBins2] pivot-bin
+    // histogram, [n_sel] pivot-bin key count (all zeroed by the score stats)
+    size_t off_hist;
+    size_t off_ctrl;    // uint32 [n_sel][8]            pivot bin, rank inside it
     size_t off_above;   // uint32 [n_sel][n_chunks]     keys above the pivot bin per chunk
-    size_t off_segcnt;  // uint32 [n_sel][n_chunks]     pivot-bin keys per chunk
-    size_t off_chunkoff;// uint32 [n_sel][n_chunks]     output offset per chunk
-    size_t off_seg;     // uint2  [n_sel][n_chunks * kSelChunk] pivot-bin (key, candidate)
+    size_t off_seg;     // uint2  [n_sel][n_chunks * kSelChunk] pivot-bin (key, candidate), unordered
     size_t total;
 };
 
@@ -71,19 +74,17 @@ inline void plan_select_layout(SelectPlan &p) {
     p.off_rmax = o;   o = align_up(o + sizeof(float) * (size_t)p.n_rows);
     p.off_rinvz = o;  o = align_up(o + sizeof(double) * (size_t)p.n_rows);
     p.off_r32 = o;    o = align_up(o + sizeof(float) * (size_t)p.n_sel * p.cand_stride);
-    p.off_hist = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * kSelBins);
+    p.off_hist = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * kSelHistWords);
     p.off_ctrl = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * 8);
     p.off_above = o;  o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
-    p.off_segcnt = o; o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
-    p.off_chunkoff = o; o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);
     p.off_seg = o;    o = align_up(o + 8 * (size_t)p.n_sel * p.n_chunks * kSelChunk);
     p.total = o;
 }
 
 // ---- attention ---------------------------------------------------------
-constexpr int kAttnTargetGroups = 2048;  // workgroups the split-K launch aims for
+constexpr int kAttnTargetGroups = 512;   // workgroups the split-K launch aims for
 constexpr int kAttnMinPages = 4;         // pages per split, lower bound
-constexpr int kAttnMaxPages = 64;        // pages per split, upper bound
+constexpr int kAttnMaxPages = 256;       // pages per split, upper bound
 constexpr int kAttnMaxSplits = 16384;    // split weights the merge keeps in LDS
 constexpr int kPartStride = 4;           // floats after the D outputs of a partial row: m, l, pad
 

@@ -102,9 +102,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float 
                                                                     double *__restrict__ rinvz,
                                                                     uint32_t *__restrict__ hist,
                                                                     int hist_words) {
-    // the selection histograms are filled by the next kernel; clear them here
-    if (blockIdx.x == 0)
-        for (int i = threadIdx.x; i < hist_words; i += kScoreThreads) hist[i] = 0u;
+    // the selection histograms are filled by the next kernels; clear them here
+    for (int i = blockIdx.x * kScoreThreads + threadIdx.x; i < hist_words; i += gridDim.x * kScoreThreads)
+        hist[i] = 0u;
     __shared__ float sm_f[kScoreThreads / kWave];
     __shared__ double sm_d[kScoreThreads / kWave];
     const int row = blockIdx.x;
@@ -233,14 +233,17 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
     double *rinvz = reinterpret_cast<double *>(ws + p.off_rinvz);
     float *r32 = reinterpret_cast<float *>(ws + p.off_r32);
     uint32_t *hist = reinterpret_cast<uint32_t *>(ws + p.off_hist);
-    hipError_t e = p.head_dim == 128
-                       ? launch_logits_d<128>(p, q, index, scale, logits, tmax, tsum, stream)
-                       : launch_logits_d<64>(p, q, index, scale, logits, tmax, tsum, stream);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_stats_kernel, dim3(p.n_rows), dim3(kScoreThreads), 0, stream, tmax, tsum,
-                       p.n_parts, rmax, rinvz, hist, p.n_sel * kSelBins);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(score_reduce_kernel, dim3(p.n_chunks, p.n_sel), dim3(kScoreThreads), 0, stream,
+    hipError_t e = hipSuccess;
+    if (p.n_cand > 0) {  // with no candidate the view is sink + recent only
+        e = p.head_dim == 128 ? launch_logits_d<128>(p, q, index, scale, logits, tmax, tsum, stream)
+                              : launch_logits_d<64>(p, q, index, scale, logits, tmax, tsum, stream);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(score_stats_kernel, dim3(p.n_rows), dim3(kScoreThreads), 0, stream, tmax, tsum,
+                           p.n_parts, rmax, rinvz, hist, p.n_sel * kSelHistWords);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    // at least one workgroup per row, which also marks the reserved blocks' scores
+    hipLaunchKernelGGL(score_reduce_kernel, dim3(p.n_chunks > 0 ? p.n_chunks : 1, p.n_sel), dim3(kScoreThreads), 0, stream,
                        logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
                        p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -150,14 +150,22 @@ def test_full_selection_is_dense_attention():
     check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, "f32")
 
 
-def test_exact_ties_take_lower_ids():
+# (blocks, source pages, budget blocks): ~25 ties per score value (ranked
+# pairwise), ~1,300 (radix select in LDS), and a budget that ends inside the
+# second-best score's ties
+TIE_CASES = [(500, 20, 40), (4000, 3, 40), (4000, 3, 2000)]
+
+
+@pytest.mark.parametrize("case", TIE_CASES, ids=["t25", "t1300", "t1300_deep"])
+def test_exact_ties_take_lower_ids(case):
     """Blocks whose pages hold identical keys score identically; the lower ids win."""
-    cfg = shape_cfg(2, 8, 128, 16, "bf16", 500, 0, 4, 1, W.MEAN_ALL, 40, planted=0)
-    log("[case] exact ties")
+    m, n_src, extra = case
+    cfg = shape_cfg(2, 8, 128, 16, "bf16", m, 0, 4, 1, W.MEAN_ALL, extra, planted=0)
+    log(f"[case] exact ties {case}")
     w = W.generate(cfg, 9)
     kp = w.k_pool[0].copy()
-    # every page gets the keys of one of 20 source pages: massive exact ties
-    src = np.random.default_rng(0).integers(0, 20, cfg.n_blocks)
+    # every page gets the keys of one of a few source pages: massive exact ties
+    src = np.random.default_rng(0).integers(0, n_src, cfg.n_blocks)
     kp[:] = kp[src]
     index_ref = oracle.mean_k(kp, w.block_to_page)
     rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 0, cfg.n_recent)
