@@ -196,8 +196,16 @@ def main():
     sel_bytes, attn_bytes = algorithmic_bytes(cfg)
     step_bytes = cfg.n_layers * (sel_bytes + attn_bytes)
     roofline = None
+    dist = None
     if evs:
-        attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+        attn_all = np.array([a.elapsed_time(b) for a, b in evs])
+        attn_ms = float(np.mean(attn_all))
+        # one step = between the starts of consecutive first-layer attention calls
+        starts = [evs[i * cfg.n_layers][0] for i in range(args.steps)]
+        step_all = np.array([starts[i].elapsed_time(starts[i + 1]) for i in range(len(starts) - 1)])
+        dist = {"step_ms_p10_p50_p90": [round(float(np.percentile(step_all, p)), 5) for p in (10, 50, 90)]
+                if step_all.size else None,
+                "attn_ms_p10_p50_p90": [round(float(np.percentile(attn_all, p)), 5) for p in (10, 50, 90)]}
         achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
@@ -209,6 +217,20 @@ def main():
                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                     "kernel": "kvmem_sparse_attn (attn_splitk + attn_combine)",
                     "bytes_per_launch": attn_bytes, "avg_launch_ms": round(attn_ms, 5)}
+
+    # attainable-bandwidth reference: a plain 2 GiB device-to-device copy
+    # (2 GiB read + 2 GiB written per copy), timed with events
+    src = torch.empty(1 << 29, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_ref = round(5 * 2 * src.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)
+    del src, dst
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -243,6 +265,8 @@ def main():
         "step_GBps": round(gbps, 1),
         "step_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "index_build_GBps": round(build_bytes / (build_ms * 1e-3) / 1e9, 1),
+        "timing_distribution": dist,
+        "attainable_copy_GBps": copy_ref,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -411,6 +411,235 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     }
 }
 
+// MFMA path for bf16 K/V with 16 query rows per KV head (e.g. 4 GQA heads x 4
+// query tokens).  At 16 rows the step does 16 flops per K/V byte, more than the
+// vector units sustain at full HBM rate, so both products run on the matrix
+// cores (v_mfma_f32_16x16x32_bf16).  Lane l of a wave works on query row l % 16;
+// kg = l / 16 picks its 8-element slice of each 32-long contraction.
+//   scores  S^T = K Q^T per 16 tokens: K rows come straight from memory into
+//           the A operand (lane: token l%16, 8 dims), Q^T is the B operand kept
+//           in registers.  Q is split as hi + lo bf16 (q = hi + lo to 2^-16),
+//           so the logits keep fp32 accuracy at twice the (cheap) MFMA count.
+//           Lane l receives S[row l%16][tokens 4kg .. 4kg+3] of the 16.
+//   softmax online per row in base 2; each lane holds 8 scores of its row per
+//           32-token tile, the row max is completed over the 4 kg lanes.
+//   output  O^T = V^T P^T per 32 tokens and 16 dims: P^T (B operand) is the
+//           lane's own 8 probabilities, split hi + lo; V^T (A operand) is read
+//           from a per-wave LDS copy of the tile (row pitch D + 4 halves keeps
+//           the column reads free of bank conflicts).  The contraction order of
+//           tokens is the same permutation on both sides.
+// Waves take the split's 32-token tiles in turn and are merged in LDS; one
+// partial (O, max, sum) per row is written in the format attn_combine reads.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kMfmaRows = 16;
+constexpr int kMfmaTile = 32;  // tokens per tile
+
+__device__ inline uint16_t bf16_rne(float x) {  // round to nearest even (finite x)
+    const uint32_t u = __float_as_uint(x);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+__device__ inline float bf16_val(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// hi + lo bf16 split of 8 floats
+__device__ inline void split_bf16x8(const float (&x)[8], bf16x8_t &hi, bf16x8_t &lo) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint16_t h = bf16_rne(x[j]);
+        const uint16_t l = bf16_rne(x[j] - bf16_val(h));
+        hi[j] = __builtin_bit_cast(__bf16, h);
+        lo[j] = __builtin_bit_cast(__bf16, l);
+    }
+}
+
+__device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+template <int D, int BT>
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
+    const float *__restrict__ q, const uint16_t *__restrict__ k_pool, const uint16_t *__restrict__ v_pool,
+    int64_t n_pages, const int32_t *__restrict__ view_pages, int n_sel, int n_view, int last_page_tokens,
+    int n_kv_heads, int n_q_heads, int group, int rows_total, int pages_per_split, int n_splits,
+    float qscale, float *__restrict__ part) {
+    constexpr int KC = D / 32;           // 32-long chunks of the head dimension (scores)
+    constexpr int MB = D / 16;           // 16-dim blocks of the output
+    constexpr int VP = D + 4;            // LDS row pitch of the V tile, in halves
+    constexpr int VL = kMfmaTile * D / 8 / kWave;  // 16-byte V loads per lane per tile
+    static_assert(VL * kWave * 8 == kMfmaTile * D, "V tile split over the wave");
+    __shared__ uint16_t sm_v[kAttnWaves][kMfmaTile * VP];
+    __shared__ float sm_m[kAttnWaves][kMfmaRows], sm_l[kAttnWaves][kMfmaRows];
+    __shared__ int sm_bad[kAttnWaves];
+
+    const int split = blockIdx.x, g = blockIdx.y, row0 = blockIdx.z * kMfmaRows;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r16 = lane % 16, kg = lane / 16;
+    const int32_t *vpages = view_pages + (int64_t)(n_sel == 1 ? 0 : g) * n_view;
+    const int p_begin = split * pages_per_split;
+    const int p_end = min(n_view, p_begin + pages_per_split);
+    // tokens of the split, page-major; the view's last page may be partial
+    const int n_tok = (p_end - p_begin) * BT - (p_end == n_view ? BT - last_page_tokens : 0);
+    const int n_tiles = (n_tok + kMfmaTile - 1) / kMfmaTile;
+
+    // Q^T operand: lane holds q[row r16][32c + 8kg + j] * qscale as hi + lo
+    bf16x8_t qhi[KC], qlo[KC];
+    {
+        const int row = row0 + r16, m = row / group, hh = row % group;
+        const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D + 8 * kg;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+            const float4 a = *reinterpret_cast<const float4 *>(qp + 32 * c);
+            const float4 b = *reinterpret_cast<const float4 *>(qp + 32 * c + 4);
+            const float x[8] = {a.x * qscale, a.y * qscale, a.z * qscale, a.w * qscale,
+                                b.x * qscale, b.y * qscale, b.z * qscale, b.w * qscale};
+            split_bf16x8(x, qhi[c], qlo[c]);
+        }
+    }
+    f32x4_t acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float mrun = -INFINITY, lpart = 0.f;
+    int bad = 0;
+
+    // page of split-local token s (< n_tok), or -1 if it is not a valid page
+    auto page_of = [&](int s) -> int64_t {
+        const int64_t pg = vpages[p_begin + s / BT];
+        return (pg < 0 || pg >= n_pages) ? -1 : pg;
+    };
+    // K rows of a tile: half h, lane -> token 16h + r16, dims 32c + 8kg ..
+    uint4 kx[2][KC], vx[VL];
+    bool kok[2];
+    auto load_tile = [&](int t) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int s = t * kMfmaTile + 16 * h + r16;
+            const int64_t pg = s < n_tok ? page_of(s) : -1;
+            kok[h] = pg >= 0;
+            const uint16_t *kr = k_pool + ((pg < 0 ? 0 : pg) * n_kv_heads + g) * (int64_t)BT * D +
+                                 (int64_t)(s % BT) * D + 8 * kg;
+#pragma unroll
+            for (int c = 0; c < KC; ++c) kx[h][c] = pg >= 0 ? load_stream16(kr + 32 * c) : make_uint4(0, 0, 0, 0);
+        }
+        // V rows: load i covers tokens (lane + 64 i) / (D/8), 16 bytes each
+#pragma unroll
+        for (int i = 0; i < VL; ++i) {
+            const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
+            const int s = t * kMfmaTile + x;
+            const int64_t pg = s < n_tok ? page_of(s) : -1;
+            const uint16_t *vr = v_pool + ((pg < 0 ? 0 : pg) * n_kv_heads + g) * (int64_t)BT * D +
+                                 (int64_t)(s % BT) * D + 8 * ch;
+            vx[i] = pg >= 0 ? load_stream16(vr) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    uint16_t *my_v = sm_v[wave];
+    for (int t = wave; t < n_tiles; t += kAttnWaves) {
+        load_tile(t);
+        // invalid pages inside the split's range make the partial NaN
+        {
+            const int s0 = t * kMfmaTile + r16, s1 = s0 + 16;
+            if ((s0 < n_tok && page_of(s0) < 0) || (s1 < n_tok && page_of(s1) < 0)) bad = 1;
+        }
+        // V tile to LDS (row x, 8 halves at 8ch)
+#pragma unroll
+        for (int i = 0; i < VL; ++i) {
+            const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
+            uint2 *dst = reinterpret_cast<uint2 *>(my_v + x * VP + 8 * ch);
+            dst[0] = make_uint2(vx[i].x, vx[i].y);
+            dst[1] = make_uint2(vx[i].z, vx[i].w);
+        }
+        // scores of the 32 tokens: lane gets row r16, tokens 16h + 4kg + i
+        float sc[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            f32x4_t st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                const bf16x8_t kb = as_bf16x8(kx[h][c]);
+                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qhi[c], st, 0, 0, 0);
+                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qlo[c], st, 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int s = t * kMfmaTile + 16 * h + 4 * kg + i;
+                sc[4 * h + i] = s < n_tok ? st[i] : -INFINITY;
+            }
+        }
+        // online softmax of row r16 (replicated over the 4 kg lanes)
+        float cm = sc[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) cm = fmaxf(cm, sc[j]);
+        cm = fmaxf(cm, shfl_xor_f(cm, 16));
+        cm = fmaxf(cm, shfl_xor_f(cm, 32));
+        const float mn = fmaxf(mrun, cm);
+        const float msafe = mn == -INFINITY ? 0.f : mn;
+        if (__any(mn > mrun)) {
+            const float alpha = exp2f(mrun - msafe);
+            lpart *= alpha;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) acc[mb] *= alpha;
+        }
+        mrun = mn;
+        float pr[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            pr[j] = exp2f(sc[j] - msafe);
+            lpart += pr[j];
+        }
+        bf16x8_t phi, plo;
+        split_bf16x8(pr, phi, plo);
+        // output: A = V^T (dims 16mb + r16, tokens 16(j/4) + 4kg + j%4 from LDS)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            bf16x8_t va;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int x = 16 * (j / 4) + 4 * kg + (j % 4);
+                va[j] = __builtin_bit_cast(__bf16, my_v[x * VP + 16 * mb + r16]);
+            }
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[mb], 0, 0, 0);
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[mb], 0, 0, 0);
+        }
+    }
+    // row sums over the 4 kg lanes
+    float lrun = lpart + shfl_xor_f(lpart, 16);
+    lrun += shfl_xor_f(lrun, 32);
+    // merge the waves: O^T in LDS as [wave][row][D] floats (reuses the V tiles)
+    __syncthreads();
+    float *sm_o = reinterpret_cast<float *>(&sm_v[0][0]);
+    static_assert(sizeof(float) * kAttnWaves * kMfmaRows * D <= sizeof(uint16_t) * kAttnWaves * kMfmaTile * VP,
+                  "merge buffer fits the V tiles");
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sm_o[(wave * kMfmaRows + r16) * D + 16 * mb + 4 * kg + i] = acc[mb][i];
+    if (kg == 0) {
+        sm_m[wave][r16] = mrun;
+        sm_l[wave][r16] = lrun;
+    }
+    if (lane == 0) sm_bad[wave] = 0;
+    __syncthreads();
+    if (bad) atomicOr(&sm_bad[wave], 1);
+    __syncthreads();
+    const bool any_bad = sm_bad[0] | sm_bad[1] | sm_bad[2] | sm_bad[3];
+    for (int idx = threadIdx.x; idx < kMfmaRows * D; idx += kAttnThreads) {
+        const int r = idx / D, d = idx % D;
+        float mx = sm_m[0][r];
+#pragma unroll
+        for (int w = 1; w < kAttnWaves; ++w) mx = fmaxf(mx, sm_m[w][r]);
+        float o = 0.f, l = 0.f;
+#pragma unroll
+        for (int w = 0; w < kAttnWaves; ++w) {
+            const float f = sm_m[w][r] == -INFINITY ? 0.f : exp2f(sm_m[w][r] - mx);
+            o += sm_o[(w * kMfmaRows + r) * D + d] * f;
+            l += sm_l[w][r] * f;
+        }
+        float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r) * (D + kPartStride);
+        dst[d] = any_bad ? __builtin_nanf("") : o;
+        if (d == 0) {
+            dst[D] = mx;
+            dst[D + 1] = l;
+        }
+    }
+}
+
 constexpr int kCombineThreads = 256;
 
 // One workgroup per (KV head, row).  The split weights 2^(m_s - M) are formed
@@ -503,10 +732,25 @@ hipError_t launch_row16(const AttnPlan &p, const float *q, const void *k_pool, c
     return hipGetLastError();
 }
 
+template <int D, int BT>
+hipError_t launch_mfma16(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
+                         int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
+                         hipStream_t stream) {
+    dim3 grid(p.n_splits, p.n_kv_heads, p.rows_per_head / kMfmaRows);
+    hipLaunchKernelGGL((attn_mfma16_kernel<D, BT>), grid, dim3(kAttnThreads), 0, stream, q,
+                       static_cast<const uint16_t *>(k_pool), static_cast<const uint16_t *>(v_pool), n_pages,
+                       view_pages, p.n_sel, p.n_view, p.last_page_tokens, p.n_kv_heads, p.n_q_heads,
+                       p.group, p.rows_per_head, p.pages_per_split, p.n_splits, qscale, part);
+    return hipGetLastError();
+}
+
 template <typename T, int D, int BT>
 hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const void *v, int64_t n_pages,
                      const int32_t *vp, float qscale, float *part, hipStream_t stream) {
     const int rows = p.rows_per_head;
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        if (rows % kMfmaRows == 0) return launch_mfma16<D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+    }
     if constexpr (D / Vec16<T>::N == 16) {
         if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
         if (rows % 4 == 0) return launch_row16<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);

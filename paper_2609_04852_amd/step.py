@@ -58,9 +58,12 @@ class LayerState:
         self.view_blocks = torch.empty((self.n_sel, self.n_view), dtype=torch.int32, device=self.device)
         self.view_pages = torch.empty_like(self.view_blocks)
         self.scores = torch.empty((self.n_sel, self.n_blocks), dtype=torch.float32, device=self.device)
-        ws = K.kvmem_select_workspace_bytes(g, 1, self.n_q, self.n_blocks, self.n_sink, self.n_recent,
-                                            self.mode)
-        self.select_ws = torch.empty(ws, dtype=torch.uint8, device=self.device)
+        try:
+            ws = K.kvmem_select_workspace_bytes(g, 1, self.n_q, self.n_blocks, self.n_sink, self.n_recent,
+                                                self.mode)
+            self.select_ws = torch.empty(ws, dtype=torch.uint8, device=self.device)
+        except K.KvmemError as e:  # attention-only use of a shape that selection does not take
+            self.select_ws, self.select_error = None, e
         aws = K.kvmem_sparse_attn_workspace_bytes(g, self.n_q, self.n_sel, self.n_view)
         self.attn_ws = torch.empty(aws, dtype=torch.uint8, device=self.device)
         self.out = torch.empty((self.n_q, g.n_q_heads, g.head_dim), dtype=torch.float32, device=self.device)
@@ -78,6 +81,8 @@ class LayerState:
 
     def select(self, q: torch.Tensor, with_scores: bool = True, stream=None) -> int:
         """q [1][n_q][Hq][d] (this layer).  Fills view_blocks/view_pages (and scores)."""
+        if self.select_ws is None:
+            raise self.select_error
         return K.kvmem_select(self.geom, q, self.index, self.n_blocks, self.n_sink, self.n_recent,
                               self.budget, self.budget, self.mode, 0.0, self.block_to_page,
                               self.view_blocks, self.view_pages, self.select_ws,

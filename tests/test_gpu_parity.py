@@ -106,6 +106,10 @@ SHAPES = [
     (16, 32, 64, 32, "bf16", 900, 1, 9, 1, W.MEAN_ALL, 77),
     (32, 64, 128, 16, "bf16", 300, 0, 4, 1, W.MAX_GROUP, 50),
     (2, 2, 128, 64, "f32", 129, 0, 1, 1, W.MEAN_ALL, 1),
+    # 16 query rows per KV head (bf16): the matrix-core attention path
+    (2, 16, 128, 16, "bf16", 700, 0, 5, 2, W.MEAN_ALL, 100),
+    (4, 16, 64, 32, "bf16", 500, 1, 3, 4, W.MAX_GROUP, 60),
+    (2, 8, 128, 64, "bf16", 260, 0, 2, 4, W.MAX_GROUP, 37),
 ]
 
 
@@ -207,6 +211,23 @@ def test_deterministic():
         assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
 
+@pytest.mark.parametrize("bt,lpt", [(16, 16), (32, 5), (64, 33)])
+def test_random_views_32_rows(bt, lpt):
+    """Attention alone with 32 query rows per KV head (two 16-row groups on the
+    matrix cores), arbitrary page lists and a partial last page."""
+    cfg = shape_cfg(2, 16, 128, bt, "bf16", 300, 0, 2, 4, W.MAX_GROUP, 10)
+    log(f"[case] 32 rows per KV head, Bt={bt}, last page {lpt}")
+    w = W.generate(cfg, 21)
+    rng = np.random.default_rng(5)
+    vp = np.stack([rng.choice(cfg.n_blocks, 97, replace=False) for _ in range(2)]).astype(np.int32)
+    q = np.ascontiguousarray(w.q[0, 0])
+    o_ref, l_ref = oracle.view_attention(q, w.k_pool[0], w.v_pool[0], vp, last_page_tokens=lpt)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    out, lse = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(vp).cuda(), last_page_tokens=lpt)
+    torch.cuda.synchronize()
+    check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, "bf16")
+
+
 def test_random_views_per_head():
     """Attention alone on arbitrary page lists (one per KV head), any order."""
     cfg = shape_cfg(4, 16, 128, 32, "bf16", 800, 0, 2, 2, W.MAX_GROUP, 10)
@@ -237,6 +258,17 @@ def test_out_of_range_pages_give_nan():
     assert np.isnan(o[:, 4:]).all() and np.isfinite(o[:, :4]).all()
     o_ref, _ = oracle.view_attention(w.q[0, 0, :, :4], w.k_pool[0][:, :1], w.v_pool[0][:, :1], vp[:1])
     np.testing.assert_allclose(o[:, :4], o_ref, atol=1e-4, rtol=0)
+    # the same on the matrix-core path (16 rows per KV head, bf16)
+    cfg16 = shape_cfg(2, 16, 128, 16, "bf16", 200, 0, 2, 2, W.MAX_GROUP, 20)
+    w16 = W.generate(cfg16, 13)
+    st16 = LayerState(cfg16, w16.k_pool[0], w16.v_pool[0], w16.block_to_page)
+    q16 = np.ascontiguousarray(w16.q[0, 0])
+    out16, _ = st16.attend(torch.from_numpy(q16).cuda(), torch.from_numpy(vp).cuda())
+    torch.cuda.synchronize()
+    o16 = out16.cpu().numpy()  # [n_q][Hq][d]; heads 0..7 read KV head 0, 8..15 KV head 1
+    assert np.isnan(o16[:, 8:]).all() and np.isfinite(o16[:, :8]).all()
+    o16_ref, _ = oracle.view_attention(q16[:, :8], w16.k_pool[0][:, :1], w16.v_pool[0][:, :1], vp[:1])
+    np.testing.assert_allclose(o16[:, :8], o16_ref, atol=2e-2, rtol=0)
     b2p = w.block_to_page.copy()
     b2p[7] = -3
     st2 = LayerState(cfg, w.k_pool[0], None, b2p)
