@@ -469,6 +469,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     __shared__ float sm_m[kAttnWaves][kMfmaRows], sm_l[kAttnWaves][kMfmaRows];
     __shared__ int sm_bad[kAttnWaves];
 
+    __shared__ int32_t sm_pg[kAttnMaxPages];
     const int split = blockIdx.x, g = blockIdx.y, row0 = blockIdx.z * kMfmaRows;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r16 = lane % 16, kg = lane / 16;
@@ -478,6 +479,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     // tokens of the split, page-major; the view's last page may be partial
     const int n_tok = (p_end - p_begin) * BT - (p_end == n_view ? BT - last_page_tokens : 0);
     const int n_tiles = (n_tok + kMfmaTile - 1) / kMfmaTile;
+    // the split's page ids, staged once (invalid ones are never read: they
+    // become page 0 and make this split's partial NaN)
+    if (threadIdx.x < kAttnWaves) sm_bad[threadIdx.x] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < p_end - p_begin; i += kAttnThreads) {
+        const int32_t pg = vpages[p_begin + i];
+        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
+        sm_pg[i] = ok ? pg : 0;
+        if (!ok) sm_bad[0] = 1;
+    }
+    __syncthreads();
+    const bool any_bad = sm_bad[0] != 0;
 
     // Q^T operand: lane holds q[row r16][32c + 8kg + j] * qscale as hi + lo
     bf16x8_t qhi[KC], qlo[KC];
@@ -497,54 +510,49 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float mrun = -INFINITY, lpart = 0.f;
-    int bad = 0;
 
-    // page of split-local token s (< n_tok), or -1 if it is not a valid page
-    auto page_of = [&](int s) -> int64_t {
-        const int64_t pg = vpages[p_begin + s / BT];
-        return (pg < 0 || pg >= n_pages) ? -1 : pg;
-    };
-    // K rows of a tile: half h, lane -> token 16h + r16, dims 32c + 8kg ..
-    uint4 kx[2][KC], vx[VL];
-    bool kok[2];
-    auto load_tile = [&](int t) {
+    // K and V of tile t (16 tokens of a half never cross a page): K half h,
+    // lane -> token 16h + r16, dims 32c + 8kg ..; V load i -> token
+    // (lane + 64 i) / (D/8), 16 bytes at dim 8 * ((lane + 64 i) % (D/8)).
+    // Tokens past the split read token 0 of the split's first page (in bounds)
+    // and are masked out of the softmax.
+    auto load_tile = [&](int t, uint4 (&kb)[2][KC], uint4 (&vb)[VL]) {
+        const uint16_t *kbase[2], *vbase[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const int s = t * kMfmaTile + 16 * h + r16;
-            const int64_t pg = s < n_tok ? page_of(s) : -1;
-            kok[h] = pg >= 0;
-            const uint16_t *kr = k_pool + ((pg < 0 ? 0 : pg) * n_kv_heads + g) * (int64_t)BT * D +
-                                 (int64_t)(s % BT) * D + 8 * kg;
-#pragma unroll
-            for (int c = 0; c < KC; ++c) kx[h][c] = pg >= 0 ? load_stream16(kr + 32 * c) : make_uint4(0, 0, 0, 0);
+            const int s0 = min(t * kMfmaTile + 16 * h, n_tok - 1);
+            const int64_t off = ((int64_t)sm_pg[s0 / BT] * n_kv_heads + g) * (int64_t)BT * D +
+                                (int64_t)(s0 % BT) * D;
+            kbase[h] = k_pool + off;
+            vbase[h] = v_pool + off;
         }
-        // V rows: load i covers tokens (lane + 64 i) / (D/8), 16 bytes each
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int tok = min(16 * h + r16, n_tok - 1 - (t * kMfmaTile + 16 * h) + 16 * h);
+#pragma unroll
+            for (int c = 0; c < KC; ++c)
+                kb[h][c] = load_stream16(kbase[h] + (int64_t)(tok - 16 * h) * D + 32 * c + 8 * kg);
+        }
 #pragma unroll
         for (int i = 0; i < VL; ++i) {
             const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
-            const int s = t * kMfmaTile + x;
-            const int64_t pg = s < n_tok ? page_of(s) : -1;
-            const uint16_t *vr = v_pool + ((pg < 0 ? 0 : pg) * n_kv_heads + g) * (int64_t)BT * D +
-                                 (int64_t)(s % BT) * D + 8 * ch;
-            vx[i] = pg >= 0 ? load_stream16(vr) : make_uint4(0, 0, 0, 0);
+            const int h = x / 16;
+            const int tok = min(x, n_tok - 1 - t * kMfmaTile);
+            vb[i] = load_stream16(vbase[h] + (int64_t)(tok - 16 * h) * D + 8 * ch);
         }
     };
     uint16_t *my_v = sm_v[wave];
-    for (int t = wave; t < n_tiles; t += kAttnWaves) {
-        load_tile(t);
-        // invalid pages inside the split's range make the partial NaN
-        {
-            const int s0 = t * kMfmaTile + r16, s1 = s0 + 16;
-            if ((s0 < n_tok && page_of(s0) < 0) || (s1 < n_tok && page_of(s1) < 0)) bad = 1;
-        }
-        // V tile to LDS (row x, 8 halves at 8ch)
+    // V tile to LDS (row x, 8 halves at 8ch); a wave reads only its own tile
+    auto stage_v = [&](const uint4 (&vb)[VL]) {
 #pragma unroll
         for (int i = 0; i < VL; ++i) {
             const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
             uint2 *dst = reinterpret_cast<uint2 *>(my_v + x * VP + 8 * ch);
-            dst[0] = make_uint2(vx[i].x, vx[i].y);
-            dst[1] = make_uint2(vx[i].z, vx[i].w);
+            dst[0] = make_uint2(vb[i].x, vb[i].y);
+            dst[1] = make_uint2(vb[i].z, vb[i].w);
         }
+    };
+    auto process = [&](int t, const uint4 (&kb)[2][KC]) {
         // scores of the 32 tokens: lane gets row r16, tokens 16h + 4kg + i
         float sc[8];
 #pragma unroll
@@ -552,9 +560,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             f32x4_t st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < KC; ++c) {
-                const bf16x8_t kb = as_bf16x8(kx[h][c]);
-                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qhi[c], st, 0, 0, 0);
-                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qlo[c], st, 0, 0, 0);
+                const bf16x8_t kk = as_bf16x8(kb[h][c]);
+                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qhi[c], st, 0, 0, 0);
+                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qlo[c], st, 0, 0, 0);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -597,6 +605,26 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[mb], 0, 0, 0);
             acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[mb], 0, 0, 0);
         }
+    };
+    // wave w takes tiles w, w + 4, ...; the next tile's loads are in flight
+    // while the current one is processed (its V goes to LDS first, so only
+    // one V tile is held in registers)
+    {
+        uint4 ka[2][KC], kb2[2][KC], vx[VL];
+        int t = wave;
+        if (t < n_tiles) load_tile(t, ka, vx);
+        while (t < n_tiles) {
+            stage_v(vx);
+            const int t1 = t + kAttnWaves;
+            if (t1 < n_tiles) load_tile(t1, kb2, vx);
+            process(t, ka);
+            if (t1 >= n_tiles) break;
+            stage_v(vx);
+            const int t2 = t1 + kAttnWaves;
+            if (t2 < n_tiles) load_tile(t2, ka, vx);
+            process(t1, kb2);
+            t = t2;
+        }
     }
     // row sums over the 4 kg lanes
     float lrun = lpart + shfl_xor_f(lpart, 16);
@@ -614,11 +642,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         sm_m[wave][r16] = mrun;
         sm_l[wave][r16] = lrun;
     }
-    if (lane == 0) sm_bad[wave] = 0;
     __syncthreads();
-    if (bad) atomicOr(&sm_bad[wave], 1);
-    __syncthreads();
-    const bool any_bad = sm_bad[0] | sm_bad[1] | sm_bad[2] | sm_bad[3];
     for (int idx = threadIdx.x; idx < kMfmaRows * D; idx += kAttnThreads) {
         const int r = idx / D, d = idx % D;
         float mx = sm_m[0][r];
