@@ -96,6 +96,115 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
     }
 }
 
+// 16 query rows per KV head (GQA heads x query tokens): the dot products run
+// on the fp32 matrix cores (v_mfma_f32_16x16x4f32, fp32 products and sums).
+// One wave per (index tile, KV head) as above.  Per 16-block group of the
+// tile, S^T = index Q^T: lane l loads, for each 16-dim slice c, the 4 dims
+// 16c + 4kg .. of block l%16 (kg = l/16) as one float4 from the tiled index,
+// and feeds them to 4 MFMAs whose contraction slot kg stands for those dims;
+// Q^T is the matching B operand, kept in registers.  Lane l receives the
+// logits of row l%16 for blocks 4kg .. 4kg+3 of the group.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
+    const float *__restrict__ q, const float *__restrict__ index, int n_blocks, int n_kv_heads,
+    int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
+    int n_tiles, int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
+    double *__restrict__ tsum) {
+    constexpr int RH = 16, NW = kScoreThreads / kWave, NC = D / 16;
+    __shared__ float sm_m[NW][RH];
+    __shared__ double sm_s[NW][RH];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r16 = lane % 16, kg = lane / 16;
+    const int g = blockIdx.y, l = blockIdx.z;
+    const int tile = tile_lo + blockIdx.x * NW + wave;
+    const bool tile_ok = blockIdx.x * NW + wave < n_tiles;
+    const int64_t qrow = ((int64_t)l * n_q + r16 / group) * n_q_heads + g * group + r16 % group;
+
+    // B operand: q[row r16][16c + 4kg + e] * scale
+    float qv[NC][4];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
+        qv[c][0] = v.x * scale; qv[c][1] = v.y * scale; qv[c][2] = v.z * scale; qv[c][3] = v.w * scale;
+    }
+    float s[4][4];  // [group][i]: row r16, block 16 * group + 4kg + i of the tile
+    if (tile_ok) {
+        const int64_t tiles_per_layer = index_tiles(n_blocks);
+        const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
+                                       (int64_t)(D / 4) * (kIndexTile * 4);
+        // all loads of the tile first, then four independent MFMA chains
+        float4 x[4][NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int gb = 0; gb < 4; ++gb)
+                x[gb][c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4) +
+                                                               (16 * gb + r16) * 4);
+        __builtin_amdgcn_sched_barrier(0);  // keep every load of the tile in flight together
+        f32x4_t st[4];
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb) st[gb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int gb = 0; gb < 4; ++gb)
+                    st[gb] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[gb][c][e], qv[c][e], st[gb], 0, 0, 0);
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[gb][i] = st[gb][i];
+    }
+    // logits (4 consecutive blocks per lane and group) and per-row stats
+    const int64_t b0 = (int64_t)tile * kIndexTile;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int gb = 0; gb < 4; ++gb) {
+        const int64_t c0 = b0 + 16 * gb + 4 * kg - n_sink;  // candidate of i = 0
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bool ok = tile_ok && c0 + i >= 0 && c0 + i < n_cand;
+            if (ok) logits[qrow * cand_stride + c0 + i] = s[gb][i];
+            mx = fmaxf(mx, ok ? s[gb][i] : -INFINITY);
+        }
+    }
+    mx = fmaxf(mx, shfl_xor_f(mx, 16));
+    mx = fmaxf(mx, shfl_xor_f(mx, 32));
+    double e = 0.0;
+    if (mx != -INFINITY) {
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb) {
+            const int64_t c0 = b0 + 16 * gb + 4 * kg - n_sink;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (tile_ok && c0 + i >= 0 && c0 + i < n_cand) e += (double)expf(s[gb][i] - mx);
+        }
+    }
+    e += __shfl_xor(e, 16, kWave);
+    e += __shfl_xor(e, 32, kWave);
+    if (kg == 0) {
+        sm_m[wave][r16] = mx;
+        sm_s[wave][r16] = e;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < RH) {
+        const int r = threadIdx.x;
+        const int64_t qr = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
+        float m = sm_m[0][r];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) m = fmaxf(m, sm_m[w][r]);
+        double sum = 0.0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            if (sm_m[w][r] != -INFINITY) sum += sm_s[w][r] * exp((double)sm_m[w][r] - (double)m);
+        tmax[qr * n_parts + blockIdx.x] = m;
+        tsum[qr * n_parts + blockIdx.x] = sum;
+    }
+}
+
 __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float *__restrict__ tmax,
                                                                     const double *__restrict__ tsum,
                                                                     int n_parts, float *__restrict__ rmax,
@@ -216,7 +325,14 @@ hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *ind
         case 2: return launch_logits<D, 2>(p, q, index, scale, logits, tmax, tsum, stream);
         case 4: return launch_logits<D, 4>(p, q, index, scale, logits, tmax, tsum, stream);
         case 8: return launch_logits<D, 8>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 16: return launch_logits<D, 16>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 16: {
+            dim3 grid(p.n_parts, p.n_kv_heads, p.n_layers);
+            hipLaunchKernelGGL((score_logits_mfma16_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
+                               p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
+                               (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
+                               tsum);
+            return hipGetLastError();
+        }
         default: return hipErrorInvalidValue;
     }
 }
