@@ -205,7 +205,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     constexpr int UNITS = BT / 16;     // 16-token units per page
     __shared__ float sm_o[kAttnWaves][RH][D];
     __shared__ float sm_m[kAttnWaves][RH], sm_l[kAttnWaves][RH];
-    __shared__ int sm_bad[kAttnWaves];
+    __shared__ int sm_bad;
+    __shared__ int32_t sm_pg[kAttnMaxPages];
 
     const int split = blockIdx.x, g = blockIdx.y, row0 = blockIdx.z * RH;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -214,6 +215,17 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     const int32_t *vpages = view_pages + (int64_t)(n_sel == 1 ? 0 : g) * n_view;
     const int p_begin = split * pages_per_split;
     const int p_end = min(n_view, p_begin + pages_per_split);
+    // the split's page ids, staged once (invalid ones are never read: they
+    // become page 0 and make this split's partial NaN)
+    if (threadIdx.x == 0) sm_bad = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < p_end - p_begin; i += kAttnThreads) {
+        const int32_t pg = vpages[p_begin + i];
+        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
+        sm_pg[i] = ok ? pg : 0;
+        if (!ok) sm_bad = 1;
+    }
+    __syncthreads();
 
     float qr[RH][VEC];
 #pragma unroll
@@ -233,27 +245,30 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
 #pragma unroll
         for (int e = 0; e < VEC; ++e) o[r][e] = 0.f;
     float m_own = -INFINITY, l_own = 0.f;
-    int bad = 0;
 
     // unit u of this wave: page p_begin + wave + 4*(u / UNITS), tokens 16*(u % UNITS) ...
     const int n_my_pages = p_end - p_begin - wave > 0 ? (p_end - p_begin - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int n_units = n_my_pages * UNITS;
+    // Loads are unconditional (all in flight together): a token past the
+    // page's valid ones reads token 0 of the page and is zeroed afterwards, so
+    // whatever the pool holds there never reaches the sums.
     auto fetch = [&](int u, uint4 (&kr)[4], uint4 (&vr)[4], int &ntok_out) {
         const int pi = p_begin + wave + kAttnWaves * (u / UNITS);
         const int t0 = 16 * (u % UNITS);
-        const int64_t page = vpages[pi];
-        const bool ok = page >= 0 && page < n_pages;
-        bad |= ok ? 0 : 1;
-        const int ntok = ok ? (pi == n_view - 1 ? last_page_tokens : BT) - t0 : 0;
+        const int64_t page = sm_pg[pi - p_begin];
+        const int ntok = (pi == n_view - 1 ? last_page_tokens : BT) - t0;
         ntok_out = ntok;
-        const int64_t off = ((ok ? page : 0) * n_kv_heads + g) * (int64_t)BT * D + (int64_t)t0 * D + lp * VEC;
+        const int64_t off = (page * n_kv_heads + g) * (int64_t)BT * D + (int64_t)t0 * D + lp * VEC;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int t = 4 * i + lg;
-            if (t < ntok) {
-                kr[i] = load_stream16(k_pool + off + (int64_t)t * D);
-                vr[i] = load_stream16(v_pool + off + (int64_t)t * D);
-            } else {
+            const int64_t to = (int64_t)(t < ntok ? t : -t0) * D;
+            kr[i] = load_stream16(k_pool + off + to);
+            vr[i] = load_stream16(v_pool + off + to);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (4 * i + lg >= ntok) {
                 kr[i] = make_uint4(0u, 0u, 0u, 0u);
                 vr[i] = make_uint4(0u, 0u, 0u, 0u);
             }
@@ -385,11 +400,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
             sm_l[wave][r] = l;
         }
     }
-    if (lane == 0) sm_bad[wave] = 0;
     __syncthreads();
-    if (bad) atomicOr(&sm_bad[wave], 1);
-    __syncthreads();
-    const bool any_bad = sm_bad[0] | sm_bad[1] | sm_bad[2] | sm_bad[3];
+    const bool any_bad = sm_bad != 0;
     for (int idx = threadIdx.x; idx < RH * D; idx += kAttnThreads) {
         const int r = idx / D, d = idx % D;
         float mx = sm_m[0][r];

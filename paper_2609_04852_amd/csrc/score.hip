@@ -241,31 +241,37 @@ __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float 
     }
 }
 
-// Block relevance for one selection row and one chunk of kSelChunk candidates
-// (4 per thread, float4 loads of every contributing logit row):
+// Block relevance for one selection row and kReduceCols * 4 candidates:
+// thread (slice rs, column col) sums every 4th contributing logit row for the
+// 4 candidates of its column (float4 loads), the 4 slices are then combined in
+// LDS in a fixed order:
 //   mean-all:  R_b = (1/(L*Hq)) * sum over every (l, m, h) row of p  (Eq. 10)
 //   group-max: R[l][g][b] = max over the (m, h in g) rows of layer l of p
 // with p = exp(s - max_row) / Z_row summed in fp64.  R is rounded once to fp32.
 // Each workgroup also histograms the selection key (bits(R) + 1) of its
 // candidates by bits 30..19 in LDS and adds the non-empty bins to the row's
 // global histogram, which the selection stages start from.
+constexpr int kReduceCols = kScoreThreads / 4;  // float4 columns per workgroup
+constexpr int kReduceCands = 4 * kReduceCols;
+
 __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     const float *__restrict__ logits, const float *__restrict__ rmax,
     const double *__restrict__ rinvz, int n_layers, int n_q, int n_q_heads, int n_kv_heads,
     int group, int n_blocks, int n_sink, int n_cand, int64_t cand_stride, int mode,
     float *__restrict__ r32, float *__restrict__ scores, uint32_t *__restrict__ hist) {
     __shared__ uint32_t lh[kSelBins];
+    __shared__ double sm_acc[4][kReduceCols][4];
     const int sel = blockIdx.y;
+    const int col = threadIdx.x % kReduceCols, rs = threadIdx.x / kReduceCols;
     for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads) lh[i] = 0u;
-    __syncthreads();
-    const int c0 = blockIdx.x * kSelChunk + 4 * threadIdx.x;
+    const int c0 = blockIdx.x * kReduceCands + 4 * col;
+    // mean-all: every (l, m, h) row; group-max: the (m, h in g) rows of layer l
+    const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
+    const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
     if (c0 < n_cand) {
-        double acc[4] = {0.0, 0.0, 0.0, 0.0};
-        // mean-all: every (l, m, h) row; group-max: the (m, h in g) rows of layer l
-        const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
-        const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
 #pragma unroll 8
-        for (int i = 0; i < nr; ++i) {
+        for (int i = rs; i < nr; i += 4) {
             const int64_t row = mode == 0 ? (int64_t)i
                                           : ((int64_t)l * n_q + i / group) * n_q_heads + g * group + i % group;
             const float4 x = *reinterpret_cast<const float4 *>(logits + row * cand_stride + c0);
@@ -279,10 +285,22 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
                 else acc[e] = pr > acc[e] ? pr : acc[e];
             }
         }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sm_acc[rs][col][e] = acc[e];
+    __syncthreads();
+    if (rs == 0 && c0 < n_cand) {
         float r[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            r[e] = mode == 0 ? (float)(acc[e] / (double)(n_layers * n_q_heads)) : (float)acc[e];
+        for (int e = 0; e < 4; ++e) {
+            double a = sm_acc[0][col][e];
+#pragma unroll
+            for (int k = 1; k < 4; ++k) {
+                const double b = sm_acc[k][col][e];
+                a = mode == 0 ? a + b : (b > a ? b : a);
+            }
+            r[e] = mode == 0 ? (float)(a / (double)(n_layers * n_q_heads)) : (float)a;
+        }
         float *dst = r32 + (int64_t)sel * cand_stride + c0;
         *reinterpret_cast<float4 *>(dst) = make_float4(r[0], r[1], r[2], r[3]);
 #pragma unroll
@@ -359,7 +377,8 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     // at least one workgroup per row, which also marks the reserved blocks' scores
-    hipLaunchKernelGGL(score_reduce_kernel, dim3(p.n_chunks > 0 ? p.n_chunks : 1, p.n_sel), dim3(kScoreThreads), 0, stream,
+    const int n_red = (p.n_cand + kReduceCands - 1) / kReduceCands;
+    hipLaunchKernelGGL(score_reduce_kernel, dim3(n_red > 0 ? n_red : 1, p.n_sel), dim3(kScoreThreads), 0, stream,
                        logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
                        p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;
