@@ -423,10 +423,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     }
 }
 
-// MFMA path for bf16 K/V with 16 query rows per KV head (e.g. 4 GQA heads x 4
-// query tokens).  At 16 rows the step does 16 flops per K/V byte, more than the
-// vector units sustain at full HBM rate, so both products run on the matrix
-// cores (v_mfma_f32_16x16x32_bf16).  Lane l of a wave works on query row l % 16;
+// MFMA path for bf16 K/V with 4 or more query rows per KV head (e.g. 4 GQA
+// heads x 4 query tokens), in tiles of 16 rows (a partial last tile is padded
+// with zero queries that are never written).  At 16 rows the step does 16
+// flops per K/V byte, more than the vector units sustain at full HBM rate, so
+// both products run on the matrix cores (v_mfma_f32_16x16x32_bf16); with
+// fewer rows the matrix cores still leave the vector units freer than the
+// vector kernel does.  Lane l of a wave works on query row l % 16;
 // kg = l / 16 picks its 8-element slice of each 32-long contraction.
 //   scores  S^T = K Q^T per 16 tokens: K rows come straight from memory into
 //           the A operand (lane: token l%16, 8 dims), Q^T is the B operand kept
@@ -505,16 +508,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     const bool any_bad = sm_bad[0] != 0;
 
     // Q^T operand: lane holds q[row r16][32c + 8kg + j] * qscale as hi + lo
+    // (rows past rows_total pad the 16-row tile with zeros and are not written)
     bf16x8_t qhi[KC], qlo[KC];
     {
-        const int row = row0 + r16, m = row / group, hh = row % group;
+        const int row = min(row0 + r16, rows_total - 1), m = row / group, hh = row % group;
+        const float qs = row0 + r16 < rows_total ? qscale : 0.f;
         const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D + 8 * kg;
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
             const float4 a = *reinterpret_cast<const float4 *>(qp + 32 * c);
             const float4 b = *reinterpret_cast<const float4 *>(qp + 32 * c + 4);
-            const float x[8] = {a.x * qscale, a.y * qscale, a.z * qscale, a.w * qscale,
-                                b.x * qscale, b.y * qscale, b.z * qscale, b.w * qscale};
+            const float x[8] = {a.x * qs, a.y * qs, a.z * qs, a.w * qs, b.x * qs, b.y * qs, b.z * qs, b.w * qs};
             split_bf16x8(x, qhi[c], qlo[c]);
         }
     }
@@ -655,7 +659,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         sm_l[wave][r16] = lrun;
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < kMfmaRows * D; idx += kAttnThreads) {
+    const int rows_here = min(kMfmaRows, rows_total - row0);
+    for (int idx = threadIdx.x; idx < rows_here * D; idx += kAttnThreads) {
         const int r = idx / D, d = idx % D;
         float mx = sm_m[0][r];
 #pragma unroll
@@ -772,7 +777,7 @@ template <int D, int BT>
 hipError_t launch_mfma16(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
                          int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
                          hipStream_t stream) {
-    dim3 grid(p.n_splits, p.n_kv_heads, p.rows_per_head / kMfmaRows);
+    dim3 grid(p.n_splits, p.n_kv_heads, (p.rows_per_head + kMfmaRows - 1) / kMfmaRows);
     hipLaunchKernelGGL((attn_mfma16_kernel<D, BT>), grid, dim3(kAttnThreads), 0, stream, q,
                        static_cast<const uint16_t *>(k_pool), static_cast<const uint16_t *>(v_pool), n_pages,
                        view_pages, p.n_sel, p.n_view, p.last_page_tokens, p.n_kv_heads, p.n_q_heads,
@@ -785,7 +790,8 @@ hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const voi
                      const int32_t *vp, float qscale, float *part, hipStream_t stream) {
     const int rows = p.rows_per_head;
     if constexpr (std::is_same<T, uint16_t>::value) {
-        if (rows % kMfmaRows == 0) return launch_mfma16<D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        // bf16 with 4 or more rows per KV head: matrix cores (rows padded to 16)
+        if (rows >= 4) return launch_mfma16<D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
     }
     if constexpr (D / Vec16<T>::N == 16) {
         if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
