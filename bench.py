@@ -24,7 +24,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 ATTN_SOURCES = ["paper_2609_04852_amd/csrc/attn.hip", "paper_2609_04852_amd/csrc/kvmem_device.h",
                 "paper_2609_04852_amd/csrc/kvmem_internal.h"]
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "attn_splitk_1m_traffic.json")
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "sparse_attn_1m_traffic.json")
 
 
 def parse():
@@ -215,7 +215,7 @@ def main():
                 traffic = tr.get("hbm_bytes_per_launch")
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
-                    "kernel": "kvmem_sparse_attn (attn_splitk + attn_combine)",
+                    "kernel": "kvmem_sparse_attn (split-K attention + attn_combine)",
                     "bytes_per_launch": attn_bytes, "avg_launch_ms": round(attn_ms, 5)}
 
     # attainable-bandwidth reference: a plain 2 GiB device-to-device copy

@@ -97,14 +97,18 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
 }
 
 // 16 query rows per KV head (GQA heads x query tokens): the dot products run
-// on the fp32 matrix cores (v_mfma_f32_16x16x4f32, fp32 products and sums).
-// One wave per (index tile, KV head) as above.  Per 16-block group of the
-// tile, S^T = index Q^T: lane l loads, for each 16-dim slice c, the 4 dims
-// 16c + 4kg .. of block l%16 (kg = l/16) as one float4 from the tiled index,
-// and feeds them to 4 MFMAs whose contraction slot kg stands for those dims;
-// Q^T is the matching B operand, kept in registers.  Lane l receives the
-// logits of row l%16 for blocks 4kg .. 4kg+3 of the group.
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
+// on the fp64 matrix cores (v_mfma_f64_16x16x4f64).  The fp32 inputs widen
+// exactly, their products are exact in fp64 and the sums barely round, so the
+// logit is the fp32 rounding of the exact dot product (the vector kernel's
+// fp32 accumulation, and the fp32 matrix cores even more, lose a few ulps at
+// the logit magnitudes of clustered keys, which the selection's 1e-5 band
+// cannot afford).  One wave per (index tile, KV head) as above.  Per 16-block
+// group of the tile, S^T = index Q^T: lane l loads, for each 16-dim slice c,
+// the 4 dims 16c + 4kg .. of block l%16 (kg = l/16) as one float4 from the
+// tiled index and feeds them to 4 MFMAs whose contraction slot kg stands for
+// those dims; Q^T is the matching B operand, kept in registers.  Lane l
+// receives the logits of row l%16 for blocks kg, kg+4, kg+8, kg+12 of the group.
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
 __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
@@ -122,14 +126,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     const bool tile_ok = blockIdx.x * NW + wave < n_tiles;
     const int64_t qrow = ((int64_t)l * n_q + r16 / group) * n_q_heads + g * group + r16 % group;
 
-    // B operand: q[row r16][16c + 4kg + e] * scale
+    // B operand: q[row r16][16c + 4kg + e] (the scale is applied to the sum)
     float qv[NC][4];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
         const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
-        qv[c][0] = v.x * scale; qv[c][1] = v.y * scale; qv[c][2] = v.z * scale; qv[c][3] = v.w * scale;
+        qv[c][0] = v.x; qv[c][1] = v.y; qv[c][2] = v.z; qv[c][3] = v.w;
     }
-    float s[4][4];  // [group][i]: row r16, block 16 * group + 4kg + i of the tile
+    float s[4][4];  // [group][i]: row r16, block 16 * group + kg + 4i of the tile
     if (tile_ok) {
         const int64_t tiles_per_layer = index_tiles(n_blocks);
         const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
@@ -143,31 +147,32 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
                 x[gb][c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4) +
                                                                (16 * gb + r16) * 4);
         __builtin_amdgcn_sched_barrier(0);  // keep every load of the tile in flight together
-        f32x4_t st[4];
+        f64x4_t st[4];
 #pragma unroll
-        for (int gb = 0; gb < 4; ++gb) st[gb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
                 for (int gb = 0; gb < 4; ++gb)
-                    st[gb] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[gb][c][e], qv[c][e], st[gb], 0, 0, 0);
+                    st[gb] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)x[gb][c][e], (double)qv[c][e], st[gb],
+                                                                  0, 0, 0);
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) s[gb][i] = st[gb][i];
+            for (int i = 0; i < 4; ++i) s[gb][i] = (float)(st[gb][i] * (double)scale);
     }
     // logits (4 consecutive blocks per lane and group) and per-row stats
     const int64_t b0 = (int64_t)tile * kIndexTile;
     float mx = -INFINITY;
 #pragma unroll
     for (int gb = 0; gb < 4; ++gb) {
-        const int64_t c0 = b0 + 16 * gb + 4 * kg - n_sink;  // candidate of i = 0
+        const int64_t c0 = b0 + 16 * gb + kg - n_sink;  // candidate of i = 0
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const bool ok = tile_ok && c0 + i >= 0 && c0 + i < n_cand;
-            if (ok) logits[qrow * cand_stride + c0 + i] = s[gb][i];
+            const bool ok = tile_ok && c0 + 4 * i >= 0 && c0 + 4 * i < n_cand;
+            if (ok) logits[qrow * cand_stride + c0 + 4 * i] = s[gb][i];
             mx = fmaxf(mx, ok ? s[gb][i] : -INFINITY);
         }
     }
@@ -177,10 +182,10 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     if (mx != -INFINITY) {
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) {
-            const int64_t c0 = b0 + 16 * gb + 4 * kg - n_sink;
+            const int64_t c0 = b0 + 16 * gb + kg - n_sink;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                if (tile_ok && c0 + i >= 0 && c0 + i < n_cand) e += (double)expf(s[gb][i] - mx);
+                if (tile_ok && c0 + 4 * i >= 0 && c0 + 4 * i < n_cand) e += (double)expf(s[gb][i] - mx);
         }
     }
     e += __shfl_xor(e, 16, kWave);
