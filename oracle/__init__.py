@@ -53,6 +53,10 @@ def _load():
     lib.oracle_masked_dense_attention.argtypes = [ci, ci, ci, ci, ci, ci, P, P, P, i64, P, i32, P,
                                                   ci, i32, i32, dbl, P, P]
     lib.oracle_masked_dense_attention.restype = ci
+    lib.oracle_rope.argtypes = [i64, ci, P, P, dbl, P]
+    lib.oracle_rope.restype = ci
+    lib.oracle_mean_k_rope.argtypes = [ci, ci, ci, ci, P, i64, P, P, dbl, i32, i32, P]
+    lib.oracle_mean_k_rope.restype = ci
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ci
     _lib = lib
@@ -103,6 +107,67 @@ def mean_k(k_pool, block_to_page, first_block=0, n_blocks=None, index=None):
                                b2p.ctypes.data, first_block, n_blocks, index.ctypes.data)
     _check(rc, "mean_k")
     return index
+
+
+def rope(x, pos, base):
+    """RoPE, rotate-half form (Sec. 4.3 / 4.4 position handling): rows of x [..., d]
+    rotated to positions pos (broadcast over the leading dims, any sign).  fp64."""
+    x = np.asarray(x, np.float64)
+    d = x.shape[-1]
+    pos = np.broadcast_to(np.asarray(pos, np.int64), x.shape[:-1])
+    xr = np.ascontiguousarray(x.reshape(-1, d))
+    pr = np.ascontiguousarray(pos.reshape(-1))
+    out = np.empty_like(xr)
+    rc = _load().oracle_rope(xr.shape[0], d, xr.ctypes.data, pr.ctypes.data, float(base), out.ctypes.data)
+    _check(rc, "rope")
+    return out.reshape(x.shape)
+
+
+def mean_k_rope(k_pool, block_to_page, base, block_pos=None, first_block=0, n_blocks=None, index=None):
+    """Eq. 9 from keys that carry RoPE: token t of block b sits at block_pos[b] + t
+    (None: b * Bt + t) and is rotated back before the mean.  Returns index [M][Hkv][d]."""
+    k_pool, is_bf16 = _pool(k_pool)
+    n_pages, hkv, bt, d = k_pool.shape
+    b2p = _c(block_to_page, np.int32)
+    m = b2p.shape[0]
+    if n_blocks is None:
+        n_blocks = m - first_block
+    if index is None:
+        index = np.zeros((m, hkv, d), np.float32)
+    bp = None if block_pos is None else _c(np.asarray(block_pos, np.int64), np.int64)
+    if bp is not None and bp.shape != (m,):
+        raise ValueError("block_pos must have one entry per block")
+    if first_block < 0 or n_blocks < 0 or first_block + n_blocks > m:
+        raise ValueError("block range out of bounds")
+    rc = _load().oracle_mean_k_rope(hkv, bt, d, is_bf16, k_pool.ctypes.data, n_pages, b2p.ctypes.data,
+                                    None if bp is None else bp.ctypes.data, float(base), first_block,
+                                    n_blocks, index.ctypes.data)
+    _check(rc, "mean_k_rope")
+    return index
+
+
+def to_bf16_bits(x):
+    """Round fp32 (or fp64 via fp32) values to bf16 bits, to nearest even (finite values)."""
+    u = np.ascontiguousarray(np.asarray(x, np.float32)).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def from_bf16_bits(b):
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def materialize(raw_k_pool, v_pool, src_pages, positions, base):
+    """Execution-view materialisation (Sec. 4.4, Sec. 5.3): block i takes page
+    src_pages[i] of the position-independent K pool; its token t is re-encoded at
+    positions[i] + t.  Returns (K [n][Hkv][Bt][d] fp64, V [n][Hkv][Bt][d] as stored)."""
+    raw, _ = _pool(raw_k_pool)
+    vp, _ = _pool(v_pool)
+    src = np.asarray(src_pages, np.int64)
+    k = raw[src].astype(np.float64) if raw.dtype == np.float32 else from_bf16_bits(raw[src]).astype(np.float64)
+    bt = raw.shape[2]
+    pos = np.asarray(positions, np.int64)[:, None, None] + np.arange(bt)[None, None, :]
+    pos = np.broadcast_to(pos, k.shape[:-1])
+    return rope(k, pos, base), vp[src].copy()
 
 
 def k_eff(model_ctx_tokens, gpu_kv_tokens, block_tokens, n_blocks, n_sink, n_recent):

@@ -75,6 +75,79 @@ int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16
     return 0;
 }
 
+/* ---- Position handling (Sec. 4.3 index construction; Sec. 4.4 execution
+ * view; Sec. 5.3 copy-free assembly): RoPE in rotate-half form --------- */
+
+/* Angle of pair j at position p: p * base^(-2j/d). */
+static double rope_angle(int64_t pos, int j, int head_dim, double base) {
+    return (double)pos * pow(base, -2.0 * (double)j / (double)head_dim);
+}
+
+/* Rotate one row x[d] to position `pos` (in place): the pair (x_j, x_{j+d/2})
+ * becomes (x_j cos a - x_{j+d/2} sin a, x_j sin a + x_{j+d/2} cos a). */
+static void rope_row(double *x, int64_t pos, int head_dim, double base) {
+    int h = head_dim / 2;
+    for (int j = 0; j < h; ++j) {
+        double a = rope_angle(pos, j, head_dim, base);
+        double c = cos(a), s = sin(a);
+        double x0 = x[j], x1 = x[j + h];
+        x[j] = x0 * c - x1 * s;
+        x[j + h] = x0 * s + x1 * c;
+    }
+}
+
+int oracle_rope(int64_t n_rows, int head_dim, const double *x, const int64_t *pos, double base,
+                double *out) {
+    if (!x || !pos || !out || n_rows < 0 || head_dim <= 0 || head_dim % 2 || !(base > 0.0)) return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < n_rows; ++r) {
+        double *y = out + r * head_dim;
+        if (y != x + r * head_dim) memcpy(y, x + r * head_dim, sizeof(double) * (size_t)head_dim);
+        rope_row(y, pos[r], head_dim, base);
+    }
+    return 0;
+}
+
+int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+                       const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
+                       const int64_t *block_pos, double base, int32_t first_block, int32_t n_blocks,
+                       float *index) {
+    if (!k_pool || !block_to_page || !index || n_kv_heads <= 0 || block_tokens <= 0 ||
+        head_dim <= 0 || head_dim % 2 || first_block < 0 || n_blocks < 0 || !(base > 0.0))
+        return -1;
+    for (int32_t i = 0; i < n_blocks; ++i) {
+        int64_t page = block_to_page[first_block + i];
+        if (page < 0 || page >= n_pages) return -1;
+    }
+#pragma omp parallel
+    {
+        double *row = (double *)malloc(sizeof(double) * (size_t)head_dim);
+        double *sum = (double *)malloc(sizeof(double) * (size_t)head_dim);
+#pragma omp for schedule(static)
+        for (int32_t i = 0; i < n_blocks; ++i) {
+            int32_t b = first_block + i;
+            int64_t page = block_to_page[b];
+            int64_t p0 = block_pos ? block_pos[b] : (int64_t)b * block_tokens;
+            for (int g = 0; g < n_kv_heads; ++g) {
+                for (int j = 0; j < head_dim; ++j) sum[j] = 0.0;
+                for (int t = 0; t < block_tokens; ++t) {
+                    /* the stored key carries RoPE at p0 + t: rotate it back */
+                    for (int j = 0; j < head_dim; ++j)
+                        row[j] = load_elem(k_pool, kv_is_bf16,
+                                           pool_offset(page, g, t, j, n_kv_heads, block_tokens, head_dim));
+                    rope_row(row, -(p0 + t), head_dim, base);
+                    for (int j = 0; j < head_dim; ++j) sum[j] += row[j];
+                }
+                for (int j = 0; j < head_dim; ++j)
+                    index[((int64_t)b * n_kv_heads + g) * head_dim + j] = (float)(sum[j] / (double)block_tokens);
+            }
+        }
+        free(row);
+        free(sum);
+    }
+    return 0;
+}
+
 /* ---- Eq. 5 / Eq. 7: active budget -> number of selectable blocks ------- */
 int64_t oracle_k_eff(int64_t model_ctx_tokens, int64_t gpu_kv_tokens, int block_tokens,
                      int32_t n_blocks, int32_t n_sink, int32_t n_recent) {

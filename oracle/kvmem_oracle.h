@@ -17,8 +17,10 @@
  * Readings of the paper that these functions fix (also listed in the design
  * notes): candidates exclude the sink and recent blocks; ties are broken by the
  * lower block id; the ranking decision is taken on scores rounded to fp32;
- * query head h belongs to KV head floor(h / G); no positional encoding is
- * applied (keys and queries are taken as position independent).
+ * query head h belongs to KV head floor(h / G); scoring and attention take
+ * keys and queries as given (position independent, or already encoded at the
+ * positions the caller chose); the RoPE functions below move them between
+ * frames.
  *
  * Return value of every int function: 0 on success, -1 on bad arguments.
  */
@@ -43,6 +45,30 @@ extern "C" {
 int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
                   const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                   int32_t first_block, int32_t n_blocks, float *index);
+
+/* Positional encoding (Sec. 4.3: keys are freed of RoPE before the index is
+ * built; Sec. 4.4 and Sec. 5.3: selected blocks are given contiguous positions
+ * in the compact execution window and their keys re-encoded there).  The
+ * paper does not print the RoPE variant; these functions use the rotate-half
+ * form of the Qwen models its engine serves: for j < d/2 the pair
+ * (x_j, x_{j+d/2}) at position p is rotated by the angle p * base^(-2j/d),
+ *   (x_j, x_{j+d/2}) -> (x_j cos a - x_{j+d/2} sin a, x_j sin a + x_{j+d/2} cos a).
+ * A negative position undoes the rotation.  Angles, cos and sin in fp64. */
+
+/* Rotate each row of x [n_rows][head_dim] to the position pos[row]; out may
+ * alias x. */
+int oracle_rope(int64_t n_rows, int head_dim, const double *x, const int64_t *pos, double base,
+                double *out);
+
+/* Eq. 9 over position-independent keys, from a pool whose keys carry RoPE:
+ * token t of block b sits at position block_pos[b] + t (block_pos NULL: the
+ * block's original frame b * block_tokens + t), is rotated back to position
+ * 0 in fp64, and the block's mean is rounded once to fp32 (index layout as
+ * oracle_mean_k). */
+int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+                       const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
+                       const int64_t *block_pos, double base, int32_t first_block, int32_t n_blocks,
+                       float *index);
 
 /* Eq. 5 and Eq. 7 (Sec. 3.1): B_a = min(B_model, B_gpu); the mandatory context
  * is the sink and recent blocks; the remaining budget holds

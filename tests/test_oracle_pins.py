@@ -409,3 +409,93 @@ class TestWorkload:
             r = oracle.block_relevance(w.q[0], index, 0, c.n_recent)
             vb, _ = oracle.select(r, 0, c.n_recent, c.top_k, w.block_to_page)
             assert set(w.planted.tolist()) <= set(vb[0].tolist())
+
+
+# ---- Position handling: RoPE removal for the index (Sec. 4.3) and re-encoding
+# at compact positions in the execution view (Sec. 4.4, Sec. 5.3) ----------
+class TestRope:
+    def test_d2_is_multiplication_by_unit_complex(self):
+        # with d = 2 the only frequency is base^0 = 1: a plane rotation by p radians
+        import cmath
+        for p in (0, 1, 5, -3, 1000, 123457):
+            z = complex(0.3, -1.7) * cmath.exp(1j * p)
+            y = oracle.rope(np.array([[0.3, -1.7]]), [p], 10000.0)[0]
+            assert abs(y[0] - z.real) < 1e-12 and abs(y[1] - z.imag) < 1e-12
+
+    def test_pairs_are_half_apart_with_geometric_frequencies(self):
+        # unit vectors show which dims pair up and at which rate they turn:
+        # e_j mixes only with e_{j+d/2}, at angle p * base^(-2j/d)
+        d, base, p = 8, 400.0, 7
+        for j in range(d // 2):
+            e = np.zeros(d)
+            e[j] = 1.0
+            y = oracle.rope(e[None], [p], base)[0]
+            a = p * base ** (-2.0 * j / d)
+            expect = np.zeros(d)
+            expect[j], expect[j + d // 2] = math.cos(a), math.sin(a)
+            np.testing.assert_allclose(y, expect, atol=1e-14)
+
+    def test_inverse_composition_norm(self):
+        x = rng(1).standard_normal((6, 64))
+        a = np.array([0, 1, 17, 4096, 262143, 1048575])
+        b = np.array([3, -1, 100, -4096, 5, 7])
+        np.testing.assert_allclose(oracle.rope(x, 0, 1e6), x, atol=0)
+        np.testing.assert_allclose(oracle.rope(oracle.rope(x, a, 1e6), -a, 1e6), x, atol=1e-12)
+        np.testing.assert_allclose(oracle.rope(oracle.rope(x, a, 1e6), b, 1e6), oracle.rope(x, a + b, 1e6),
+                                   atol=1e-9)
+        y = oracle.rope(x, a, 1e6)
+        h = 32
+        np.testing.assert_allclose(np.hypot(y[:, :h], y[:, h:]), np.hypot(x[:, :h], x[:, h:]), rtol=1e-13)
+
+    def test_dot_products_depend_only_on_relative_position(self):
+        q, k = rng(2).standard_normal((2, 128))
+        for m, n in ((10, 3), (5000, 4000), (7, 900)):
+            base_dot = oracle.rope(q, m, 1e4) @ oracle.rope(k, n, 1e4)
+            for s in (1, 333, 100000):
+                assert abs(oracle.rope(q, m + s, 1e4) @ oracle.rope(k, n + s, 1e4) - base_dot) < 1e-9
+
+    def test_mean_k_of_encoded_keys_recovers_the_raw_mean(self):
+        # keys encoded at their blocks' positions and stored in fp32: removing the
+        # encoding before the mean gives the mean of the raw keys (up to fp32 storage)
+        r = rng(3)
+        n_pages, hkv, bt, d = 40, 2, 16, 64
+        raw = r.standard_normal((n_pages, hkv, bt, d)).astype(np.float32)
+        b2p = r.permutation(n_pages).astype(np.int32)
+        for block_pos in (None, r.integers(0, 10 ** 6, n_pages)):
+            p0 = np.arange(n_pages) * bt if block_pos is None else block_pos
+            pos = np.empty((n_pages, hkv, bt), np.int64)
+            pos[b2p] = (p0[:, None, None] + np.arange(bt)[None, None, :])
+            enc = oracle.rope(raw.astype(np.float64), pos, 1e6).astype(np.float32)
+            got = oracle.mean_k_rope(enc, b2p, 1e6, block_pos=block_pos)
+            want = oracle.mean_k(raw, b2p)
+            np.testing.assert_allclose(got, want, atol=2e-6, rtol=0)
+        # and the plain index is not what you get from encoded keys (the removal matters)
+        assert np.abs(oracle.mean_k(enc, b2p) - want).max() > 0.1
+
+    def test_bf16_rounding_is_nearest_even(self):
+        x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 3.140625, 1e-3], np.float32)
+        bits = oracle.to_bf16_bits(x)
+        back = oracle.from_bf16_bits(bits)
+        # 1 + 2^-8 is a tie between 1 and 1 + 2^-7: even mantissa (1.0) wins;
+        # 1 + 3*2^-8 ties between 1 + 2^-7 and 1 + 2^-6: the even one is 1 + 2^-6
+        np.testing.assert_array_equal(back[:4], np.array([1.0, 1.0, 1.0 + 2 ** -6, -2.5], np.float32))
+        assert abs(back[5] - 1e-3) <= 2 ** -9 * 1e-3
+
+    def test_materialize_encodes_each_token_at_its_compact_position(self):
+        r = rng(4)
+        n_pages, hkv, bt, d = 12, 2, 16, 64
+        raw = r.standard_normal((n_pages, hkv, bt, d)).astype(np.float32)
+        v = r.standard_normal((n_pages, hkv, bt, d)).astype(np.float32)
+        src = np.array([5, 0, 11, 3])
+        pos = np.array([0, 16, 32, 48])  # four blocks laid out back to back
+        k_out, v_out = oracle.materialize(raw, v, src, pos, 1e6)
+        np.testing.assert_array_equal(v_out, v[src])
+        for i, p in enumerate(pos):
+            for t in (0, 7, 15):
+                np.testing.assert_allclose(k_out[i, :, t], oracle.rope(raw[src[i], :, t], p + t, 1e6), atol=0)
+        # attention logits against a query at position P only see the offset P - (p + t)
+        q = r.standard_normal(d)
+        P = 64
+        lhs = oracle.rope(q, P, 1e6) @ k_out[2, 1, 9]
+        rhs = q @ oracle.rope(raw[src[2], 1, 9], (pos[2] + 9) - P, 1e6)
+        assert abs(lhs - rhs) < 1e-9
