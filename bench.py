@@ -218,6 +218,52 @@ def main():
                     "kernel": "kvmem_sparse_attn (split-K attention + attn_combine)",
                     "bytes_per_launch": attn_bytes, "avg_launch_ms": round(attn_ms, 5)}
 
+    # position handling (Sec. 4.4, Sec. 5.3), on the last step's view of layer 0:
+    # re-encode every view block's K at compact positions from the raw keys and
+    # copy V (kvmem_materialize), move them all by one block (kvmem_rerope), and
+    # build the index from RoPE-encoded keys (kvmem_build_index_rope).  Values do
+    # not matter for the timing; the bytes are those of the whole view.
+    st = layers[0]
+    n_view = st.view_pages.shape[1]
+    page_bytes = cfg.n_kv_heads * cfg.block_tokens * cfg.head_dim * cfg.elem_bytes
+    kx = torch.empty((n_view,) + tuple(st.k_pool.shape[1:]), dtype=st.k_pool.dtype, device=dev)
+    vx = torch.empty_like(kx)
+    src = st.view_pages[0].contiguous()
+    dst = torch.arange(n_view, dtype=torch.int32, device=dev)
+    cpos = torch.arange(n_view, dtype=torch.int64, device=dev) * cfg.block_tokens
+    shift = torch.full((n_view,), cfg.block_tokens, dtype=torch.int64, device=dev)
+    rope_base = 1e6
+
+    def timed(fn, reps=10):
+        fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    mat_ms = timed(lambda: K.kvmem_materialize(st.geom, rope_base, st.k_pool, st.v_pool, src, cpos, dst, kx, vx))
+    rer_ms = timed(lambda: K.kvmem_rerope(st.geom, rope_base, kx, dst, shift))
+    irope_ms = timed(lambda: K.kvmem_build_index_rope(st.geom, st.k_pool, st.block_to_page, 0, cfg.n_blocks,
+                                                      st.index, rope_base), reps=3)
+    st.build_index()  # restore the position-independent index
+    torch.cuda.synchronize()
+    mat_bytes = 4 * n_view * page_bytes  # read K and V, write K and V
+    rer_bytes = 2 * n_view * page_bytes  # read and write K
+    irope_bytes = build_bytes // cfg.n_layers
+    position = {"view_blocks": n_view,
+                "materialize": {"ms": round(mat_ms, 4), "bytes": mat_bytes,
+                                "GBps": round(mat_bytes / (mat_ms * 1e-3) / 1e9, 1),
+                                "frac_of_peak": round(mat_bytes / (mat_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+                "rerope": {"ms": round(rer_ms, 4), "bytes": rer_bytes,
+                           "GBps": round(rer_bytes / (rer_ms * 1e-3) / 1e9, 1),
+                           "frac_of_peak": round(rer_bytes / (rer_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+                "index_from_encoded_keys": {"ms": round(irope_ms, 4), "bytes": irope_bytes,
+                                            "GBps": round(irope_bytes / (irope_ms * 1e-3) / 1e9, 1)}}
+    del kx, vx
+
     # attainable-bandwidth reference: a plain 2 GiB device-to-device copy
     # (2 GiB read + 2 GiB written per copy), timed with events
     src = torch.empty(1 << 29, dtype=torch.float32, device=dev)
@@ -266,6 +312,7 @@ def main():
         "step_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "index_build_GBps": round(build_bytes / (build_ms * 1e-3) / 1e9, 1),
         "timing_distribution": dist,
+        "position_handling": position,
         "attainable_copy_GBps": copy_ref,
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -15,6 +15,9 @@
  *   kvmem_select       Eq. 10 + selector: scores, top-k under the budget,
  *                      chronological view tables
  *   kvmem_sparse_attn  decode attention over the view's pages (split-K)
+ *   kvmem_build_index_rope, kvmem_materialize, kvmem_rerope
+ *                      position handling: index from RoPE-encoded keys,
+ *                      re-encoding of selected blocks at compact positions
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -123,6 +126,56 @@ size_t kvmem_index_bytes(const kvmem_geom *geom, int32_t n_blocks);
 kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
                                const int32_t *block_to_page, int32_t first_block,
                                int32_t n_blocks, float *index, void *stream);
+
+/* ---- Position handling (Sec. 4.3 index construction; Sec. 4.4 execution
+ * view; Sec. 5.3 copy-free assembly) ---------------------------------------
+ * RoPE in rotate-half form (the paper does not print the variant; this is the
+ * form of the Qwen models its engine serves): for j < d/2 the pair
+ * (x_j, x_{j+d/2}) at position p turns by the angle p * rope_base^(-2j/d),
+ *   (x_j, x_{j+d/2}) -> (x_j cos a - x_{j+d/2} sin a, x_j sin a + x_{j+d/2} cos a).
+ * Angles are formed and reduced in fp64 (positions up to 2^62), cos/sin and
+ * the rotation are fp32, bf16 results are rounded to nearest even.
+ * rope_base must be finite and above 1 (KVMEM_ERR_SHAPE otherwise). */
+
+/* Eq. 9 from keys that carry RoPE (Sec. 4.3: RoPE is removed before the index
+ * is built).  As kvmem_build_index, except that token t of block b is stored
+ * encoded at position block_pos[b] + t -- its "baked position" (Sec. 5.3) --
+ * and is turned back to position 0 before it enters the mean.
+ *   block_pos  dev [M] int64, or NULL for the original frame b * Bt + t
+ * Blocks whose page is outside the pool get NaN index rows. */
+kvmem_status kvmem_build_index_rope(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
+                                    const int32_t *block_to_page, const int64_t *block_pos, double rope_base,
+                                    int32_t first_block, int32_t n_blocks, float *index, void *stream);
+
+/* Execution-view materialisation (Sec. 4.4, Sec. 5.3): the keys of a block
+ * are valid only at the positions they were encoded for, so a block placed at
+ * a new compact position gets its K re-encoded from the position-independent
+ * raw K, and V copied unchanged.  For i < n_blocks:
+ *   K of page dst_pages[i] of k_dst_pool, token t  = RoPE(raw_k_pool[src_pages[i]] token t,
+ *                                                         positions[i] + t)
+ *   V of page dst_pages[i] of v_dst_pool            = v_pool[src_pages[i]]
+ *   raw_k_pool, v_pool        dev [n_src_pages][Hkv][Bt][d] kv_dtype
+ *   k_dst_pool, v_dst_pool    dev [n_dst_pages][Hkv][Bt][d] kv_dtype
+ *   src_pages, dst_pages      dev [n_blocks] int32
+ *   positions                 dev [n_blocks] int64 (first token's position)
+ * A destination page outside its pool is skipped (nothing written); a source
+ * page outside its pool makes the destination page all NaN.  Destination
+ * pages must be distinct and must not overlap the source pools. */
+kvmem_status kvmem_materialize(const kvmem_geom *geom, double rope_base, const void *raw_k_pool,
+                               const void *v_pool, int64_t n_src_pages, const int32_t *src_pages,
+                               const int64_t *positions, const int32_t *dst_pages, int32_t n_blocks,
+                               void *k_dst_pool, void *v_dst_pool, int64_t n_dst_pages, void *stream);
+
+/* Delta re-encoding in place (Sec. 4.4): a GPU-resident block whose compact
+ * position moves by delta keeps its page; its K turns by delta positions
+ * (every token by the same angle), V is untouched.  Each call rounds K again
+ * (bf16): the paper bounds the number of such steps between rebuilds from raw
+ * K (kvmem_materialize), which is the caller's policy.
+ *   k_pool           dev [n_pages][Hkv][Bt][d] kv_dtype, updated in place
+ *   pages            dev [n_list] int32 (distinct); delta_positions dev [n_list] int64
+ * Pages outside the pool are skipped. */
+kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool, int64_t n_pages,
+                          const int32_t *pages, const int64_t *delta_positions, int32_t n_list, void *stream);
 
 /* View plan (Eq. 5, Eq. 7; host only, no HIP call).  With the active budget
  * B_a = min(model_ctx_tokens, gpu_kv_tokens) and the mandatory context of

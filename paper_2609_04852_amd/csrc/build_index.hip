@@ -22,11 +22,19 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kBlocksPerStep = 4;
 
-template <typename T, int D>
+// ROPE: the stored keys carry RoPE (rotate-half form) at positions
+// block_pos[b] + t (block_pos NULL: b * block_tokens + t); each token row is
+// turned back to position 0 before it enters the sum (Sec. 4.3: the index is
+// built from position-independent keys).  The lane holding dims [j, j+VEC)
+// of one half gets the matching dims of the other half from lane lp ^ LPR/2.
+// Angles are formed and reduced in fp64 (rope_cos_sin), cos/sin and the
+// rotation in fp32.
+
+template <typename T, int D, bool ROPE>
 __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ block_to_page,
     int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens,
-    float *__restrict__ index) {
+    float *__restrict__ index, const int64_t *__restrict__ block_pos, RopeFreqs fr) {
     constexpr int VEC = Vec16<T>::N;  // elements per lane per row
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
@@ -42,12 +50,14 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const int64_t b_end = (int64_t)first_block + n_blocks;
     const int64_t b_hi = b_tile0 + kIndexTile < b_end ? b_tile0 + kIndexTile : b_end;
     const double inv = 1.0 / (double)block_tokens;
+    const int j0 = (lp % (LPR / 2)) * VEC;  // RoPE pair index of this lane's element 0
 
     // wave w reduces tile slots w, w+4, w+8, ... (kBlocksPerStep at a time)
     for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * kBlocksPerStep) {
         double acc[kBlocksPerStep][VEC];
         bool ok[kBlocksPerStep];
         const T *base[kBlocksPerStep];
+        int64_t p0[kBlocksPerStep];
 #pragma unroll
         for (int k = 0; k < kBlocksPerStep; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
@@ -57,6 +67,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
             base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D + lp * VEC;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[k][e] = 0.0;
+            p0[k] = ROPE && block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
         }
         for (int t = tg; t < block_tokens; t += TG) {
             float v[kBlocksPerStep][VEC];
@@ -67,6 +78,23 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                 } else {
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) v[k][e] = 0.f;
+                }
+            }
+            if constexpr (ROPE) {
+                const bool upper = lp >= LPR / 2;
+#pragma unroll
+                for (int k = 0; k < kBlocksPerStep; ++k) {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        const float other = __shfl_xor(v[k][e], LPR / 2, kWave);
+                        // the angle (p0 + t) * f_j, formed as one fp64 product: the
+                        // sum of the start and offset angles would round differently
+                        // at large positions
+                        float c, sn;
+                        rope_cos_sin(p0[k] + t, fr.f[j0 + e], &c, &sn);
+                        // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
+                        v[k][e] = upper ? v[k][e] * c - other * sn : v[k][e] * c + other * sn;
+                    }
                 }
             }
 #pragma unroll
@@ -107,13 +135,22 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 template <typename T, int D>
 hipError_t launch_t(int n_kv_heads, int block_tokens, const void *k_pool, int64_t n_pages,
                     const int32_t *block_to_page, int32_t first_block, int32_t n_blocks,
-                    float *index, hipStream_t stream) {
+                    float *index, hipStream_t stream, bool rope, const int64_t *block_pos,
+                    const RopeFreqs *fr) {
     const int64_t t0 = first_block / kIndexTile;
     const int64_t t1 = ((int64_t)first_block + n_blocks + kIndexTile - 1) / kIndexTile;
     dim3 grid((unsigned)(t1 - t0), (unsigned)n_kv_heads);
-    hipLaunchKernelGGL((build_index_kernel<T, D>), grid, dim3(kWaves * kWave), 0, stream,
-                       static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
-                       n_kv_heads, block_tokens, index);
+    RopeFreqs f{};
+    if (rope) {
+        f = *fr;
+        hipLaunchKernelGGL((build_index_kernel<T, D, true>), grid, dim3(kWaves * kWave), 0, stream,
+                           static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
+                           n_kv_heads, block_tokens, index, block_pos, f);
+    } else {
+        hipLaunchKernelGGL((build_index_kernel<T, D, false>), grid, dim3(kWaves * kWave), 0, stream,
+                           static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
+                           n_kv_heads, block_tokens, index, block_pos, f);
+    }
     return hipGetLastError();
 }
 
@@ -122,18 +159,18 @@ hipError_t launch_t(int n_kv_heads, int block_tokens, const void *k_pool, int64_
 hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
                               const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                               int32_t first_block, int32_t n_blocks, float *index,
-                              hipStream_t stream) {
+                              hipStream_t stream, bool rope, const int64_t *block_pos, const RopeFreqs *fr) {
     if (n_blocks == 0) return hipSuccess;
     const bool bf16 = kv_dtype == 1;
     if (head_dim == 128)
         return bf16 ? launch_t<uint16_t, 128>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                              first_block, n_blocks, index, stream)
+                                              first_block, n_blocks, index, stream, rope, block_pos, fr)
                     : launch_t<float, 128>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                           first_block, n_blocks, index, stream);
+                                           first_block, n_blocks, index, stream, rope, block_pos, fr);
     return bf16 ? launch_t<uint16_t, 64>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                         first_block, n_blocks, index, stream)
+                                         first_block, n_blocks, index, stream, rope, block_pos, fr)
                 : launch_t<float, 64>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                      first_block, n_blocks, index, stream);
+                                      first_block, n_blocks, index, stream, rope, block_pos, fr);
 }
 
 }  // namespace kvmem

@@ -186,6 +186,80 @@ kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64
                       "build_index launch");
 }
 
+kvmem_status kvmem_build_index_rope(const kvmem_geom *geom, const void *k_pool, int64_t n_pages,
+                                    const int32_t *block_to_page, const int64_t *block_pos, double rope_base,
+                                    int32_t first_block, int32_t n_blocks, float *index, void *stream) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    if (!(rope_base > 1.0) || !std::isfinite(rope_base))
+        return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
+    if (first_block < 0 || n_blocks < 0 || (int64_t)first_block + n_blocks > INT32_MAX)
+        return fail(KVMEM_ERR_SHAPE, "block range [%d, %d + %d) is invalid", first_block, first_block,
+                    n_blocks);
+    if (n_blocks == 0) return ok();
+    if (!k_pool || !block_to_page || !index)
+        return fail(KVMEM_ERR_NULL, "k_pool, block_to_page and index must be non-NULL");
+    if (n_pages <= 0) return fail(KVMEM_ERR_SHAPE, "n_pages %lld must be positive", (long long)n_pages);
+    if (!aligned16(k_pool) || !aligned16(index) || !aligned16(block_to_page) ||
+        (block_pos && !aligned16(block_pos)))
+        return fail(KVMEM_ERR_ALIGN, "k_pool, block_to_page, block_pos and index must be 16-byte aligned");
+    kvmem::RopeFreqs fr;
+    kvmem::rope_freqs(rope_base, geom->head_dim, fr);
+    return hip_status(kvmem::launch_build_index(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
+                                                geom->block_tokens, k_pool, n_pages, block_to_page,
+                                                first_block, n_blocks, index,
+                                                static_cast<hipStream_t>(stream), true, block_pos, &fr),
+                      "build_index_rope launch");
+}
+
+kvmem_status kvmem_materialize(const kvmem_geom *geom, double rope_base, const void *raw_k_pool,
+                               const void *v_pool, int64_t n_src_pages, const int32_t *src_pages,
+                               const int64_t *positions, const int32_t *dst_pages, int32_t n_blocks,
+                               void *k_dst_pool, void *v_dst_pool, int64_t n_dst_pages, void *stream) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    if (!(rope_base > 1.0) || !std::isfinite(rope_base))
+        return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
+    if (n_blocks < 0 || n_blocks > (1 << 24))
+        return fail(KVMEM_ERR_SHAPE, "n_blocks %d must be in [0, 2^24]", n_blocks);
+    if (n_blocks == 0) return ok();
+    if (!raw_k_pool || !v_pool || !src_pages || !positions || !dst_pages || !k_dst_pool || !v_dst_pool)
+        return fail(KVMEM_ERR_NULL, "pools, page lists and positions must be non-NULL");
+    if (n_src_pages <= 0 || n_dst_pages <= 0)
+        return fail(KVMEM_ERR_SHAPE, "n_src_pages and n_dst_pages must be positive");
+    if (!aligned16(raw_k_pool) || !aligned16(v_pool) || !aligned16(k_dst_pool) || !aligned16(v_dst_pool) ||
+        !aligned16(src_pages) || !aligned16(positions) || !aligned16(dst_pages))
+        return fail(KVMEM_ERR_ALIGN, "device arrays must be 16-byte aligned");
+    kvmem::RopeFreqs fr;
+    kvmem::rope_freqs(rope_base, geom->head_dim, fr);
+    return hip_status(kvmem::launch_materialize(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
+                                                geom->block_tokens, fr, raw_k_pool, v_pool, n_src_pages,
+                                                src_pages, positions, dst_pages, n_blocks, k_dst_pool,
+                                                v_dst_pool, n_dst_pages, static_cast<hipStream_t>(stream)),
+                      "materialize launch");
+}
+
+kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool, int64_t n_pages,
+                          const int32_t *pages, const int64_t *delta_positions, int32_t n_list, void *stream) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    if (!(rope_base > 1.0) || !std::isfinite(rope_base))
+        return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
+    if (n_list < 0 || n_list > (1 << 24)) return fail(KVMEM_ERR_SHAPE, "n_list %d must be in [0, 2^24]", n_list);
+    if (n_list == 0) return ok();
+    if (!k_pool || !pages || !delta_positions)
+        return fail(KVMEM_ERR_NULL, "k_pool, pages and delta_positions must be non-NULL");
+    if (n_pages <= 0) return fail(KVMEM_ERR_SHAPE, "n_pages %lld must be positive", (long long)n_pages);
+    if (!aligned16(k_pool) || !aligned16(pages) || !aligned16(delta_positions))
+        return fail(KVMEM_ERR_ALIGN, "device arrays must be 16-byte aligned");
+    kvmem::RopeFreqs fr;
+    kvmem::rope_freqs(rope_base, geom->head_dim, fr);
+    return hip_status(kvmem::launch_rope_delta(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
+                                               geom->block_tokens, fr, k_pool, n_pages, pages, delta_positions,
+                                               n_list, static_cast<hipStream_t>(stream)),
+                      "rerope launch");
+}
+
 kvmem_status kvmem_plan_view(const kvmem_geom *geom, int32_t n_blocks, int32_t n_sink_blocks,
                              int32_t n_recent_blocks, int64_t model_ctx_tokens,
                              int64_t gpu_kv_tokens, int32_t *k_eff, int32_t *n_view) {

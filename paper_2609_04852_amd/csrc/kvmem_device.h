@@ -52,6 +52,20 @@ struct Vec16<uint16_t> {
     }
 };
 
+// cos and sin of the RoPE angle pos * f (fp64).  The angle is reduced to about
+// [-pi, pi] with a two-part 2*pi (Cody-Waite, fused multiply-adds), so the
+// reduced angle is accurate to about 1e-16 rad for any fp64 angle, then cos
+// and sin are taken in fp32.
+__device__ inline void rope_cos_sin(int64_t pos, double f, float *c, float *s) {
+    constexpr double kTwoPiHi = 6.283185307179586;        // fp64 nearest to 2*pi
+    constexpr double kTwoPiLo = 2.4492935982947064e-16;   // 2*pi - kTwoPiHi
+    constexpr double kInvTwoPi = 0.15915494309189535;
+    const double a = (double)pos * f;
+    const double k = rint(a * kInvTwoPi);
+    const double r = fma(-k, kTwoPiLo, fma(-k, kTwoPiHi, a));
+    sincosf((float)r, s, c);
+}
+
 __device__ inline float shfl_xor_f(float v, int mask) { return __shfl_xor(v, mask, kWave); }
 
 // DPP lane patterns inside one 16-lane row (gfx9 encodings; row_newbcast is gfx90a+).

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+#include <math.h>
 
 namespace kvmem {
 
@@ -106,11 +107,34 @@ inline void plan_attn_layout(AttnPlan &p) {
                        (p.head_dim + kPartStride));
 }
 
+// ---- RoPE (rotate-half form) ---------------------------------------------
+// Frequencies f_j = base^(-2j/d), j < d/2, computed on the host with the same
+// expression as the definition and passed to the kernels by value.
+struct RopeFreqs {
+    double f[64];
+};
+inline void rope_freqs(double base, int head_dim, RopeFreqs &fr) {
+    for (int j = 0; j < 64; ++j) fr.f[j] = j < head_dim / 2 ? pow(base, -2.0 * (double)j / (double)head_dim) : 0.0;
+}
+
 // ---- launchers (return the launch status) -------------------------------
+// block_pos / fr are used only when rope is set: the keys carry RoPE at
+// positions block_pos[b] + t (block_pos NULL: b * block_tokens + t).
 hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
                               const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                               int32_t first_block, int32_t n_blocks, float *index,
-                              hipStream_t stream);
+                              hipStream_t stream, bool rope = false, const int64_t *block_pos = nullptr,
+                              const RopeFreqs *fr = nullptr);
+
+hipError_t launch_materialize(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
+                              const RopeFreqs &fr, const void *raw_k, const void *v_src,
+                              int64_t n_src_pages, const int32_t *src_pages, const int64_t *positions,
+                              const int32_t *dst_pages, int32_t n, void *k_dst, void *v_dst,
+                              int64_t n_dst_pages, hipStream_t stream);
+
+hipError_t launch_rope_delta(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens, const RopeFreqs &fr,
+                             void *k_pool, int64_t n_pages, const int32_t *pages, const int64_t *delta,
+                             int32_t n, hipStream_t stream);
 
 hipError_t launch_topk(const SelectPlan &p, const int32_t *block_to_page, int32_t *view_blocks,
                        int32_t *view_pages, char *workspace, hipStream_t stream);

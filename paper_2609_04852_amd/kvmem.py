@@ -79,7 +79,12 @@ def lib() -> ctypes.CDLL:
     L.kvmem_sparse_attn_workspace_bytes.argtypes = [G, i32, i32, i32]
     L.kvmem_sparse_attn_workspace_bytes.restype = sz
     L.kvmem_sparse_attn.argtypes = [G, P, i32, P, P, i64, P, i32, i32, i32, f32, P, P, P, sz, P]
-    for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_sparse_attn"):
+    dbl = ctypes.c_double
+    L.kvmem_build_index_rope.argtypes = [G, P, i64, P, P, dbl, i32, i32, P, P]
+    L.kvmem_materialize.argtypes = [G, dbl, P, P, i64, P, P, P, i32, P, P, i64, P]
+    L.kvmem_rerope.argtypes = [G, dbl, P, i64, P, P, i32, P]
+    for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_sparse_attn",
+                 "kvmem_build_index_rope", "kvmem_materialize", "kvmem_rerope"):
         getattr(L, name).restype = ctypes.c_int
     L.kvmem_last_error.argtypes = []
     L.kvmem_last_error.restype = ctypes.c_char_p
@@ -252,3 +257,58 @@ def kvmem_sparse_attn(geom: Geom, q: torch.Tensor, k_pool: torch.Tensor, v_pool:
                                    n_pages, _ptr(view_pages), n_sel, n_view, last_page_tokens, scale,
                                    _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
                                    _stream(stream)))
+
+
+def kvmem_build_index_rope(geom: Geom, k_pool: torch.Tensor, block_to_page: torch.Tensor,
+                           first_block: int, n_blocks: int, index: torch.Tensor, rope_base: float,
+                           block_pos: torch.Tensor | None = None, stream=None):
+    """kvmem_build_index for keys that carry RoPE: token t of block b sits at
+    block_pos[b] + t (None: b * Bt + t) and is turned back before the mean."""
+    _need(block_to_page, torch.int32, "block_to_page")
+    _need(index, torch.float32, "index")
+    if block_pos is not None:
+        _need(block_pos, torch.int64, "block_pos")
+        if block_pos.numel() < first_block + n_blocks:
+            raise ValueError("block_pos is shorter than the block range")
+    if not k_pool.is_cuda or not k_pool.is_contiguous():
+        raise TypeError("k_pool must be a contiguous CUDA tensor")
+    if block_to_page.numel() < first_block + n_blocks:
+        raise ValueError("block_to_page is shorter than the block range")
+    if index.numel() * 4 < kvmem_index_bytes(geom, first_block + n_blocks):
+        raise ValueError("index is smaller than the block range needs")
+    n_pages = k_pool.numel() // (geom.n_kv_heads * geom.block_tokens * geom.head_dim)
+    _check(lib().kvmem_build_index_rope(ctypes.byref(geom.c()), _ptr(k_pool), n_pages, _ptr(block_to_page),
+                                        _ptr(block_pos), float(rope_base), first_block, n_blocks, _ptr(index),
+                                        _stream(stream)))
+
+
+def kvmem_materialize(geom: Geom, rope_base: float, raw_k_pool: torch.Tensor, v_pool: torch.Tensor,
+                      src_pages: torch.Tensor, positions: torch.Tensor, dst_pages: torch.Tensor,
+                      k_dst_pool: torch.Tensor, v_dst_pool: torch.Tensor, stream=None):
+    """Re-encode the keys of src_pages at positions[i] + t into dst_pages; copy V."""
+    for t, name in ((raw_k_pool, "raw_k_pool"), (v_pool, "v_pool"), (k_dst_pool, "k_dst_pool"),
+                    (v_dst_pool, "v_dst_pool")):
+        if kv_dtype_of(t) != geom.kv_dtype or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous pool of geom.kv_dtype")
+    _need(src_pages, torch.int32, "src_pages")
+    _need(dst_pages, torch.int32, "dst_pages")
+    _need(positions, torch.int64, "positions")
+    n = src_pages.numel()
+    if dst_pages.numel() != n or positions.numel() != n:
+        raise ValueError("src_pages, dst_pages and positions must have the same length")
+    _check(lib().kvmem_materialize(ctypes.byref(geom.c()), float(rope_base), _ptr(raw_k_pool), _ptr(v_pool),
+                                   raw_k_pool.shape[0], _ptr(src_pages), _ptr(positions), _ptr(dst_pages), n,
+                                   _ptr(k_dst_pool), _ptr(v_dst_pool), k_dst_pool.shape[0], _stream(stream)))
+
+
+def kvmem_rerope(geom: Geom, rope_base: float, k_pool: torch.Tensor, pages: torch.Tensor,
+                 delta_positions: torch.Tensor, stream=None):
+    """Turn the keys of `pages` in place by delta_positions[i] positions."""
+    if kv_dtype_of(k_pool) != geom.kv_dtype or not k_pool.is_contiguous():
+        raise TypeError("k_pool must be a contiguous pool of geom.kv_dtype")
+    _need(pages, torch.int32, "pages")
+    _need(delta_positions, torch.int64, "delta_positions")
+    if delta_positions.numel() != pages.numel():
+        raise ValueError("pages and delta_positions must have the same length")
+    _check(lib().kvmem_rerope(ctypes.byref(geom.c()), float(rope_base), _ptr(k_pool), k_pool.shape[0],
+                              _ptr(pages), _ptr(delta_positions), pages.numel(), _stream(stream)))

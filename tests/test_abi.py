@@ -165,3 +165,38 @@ def test_sparse_attn_validation(L):
     assert _attn(L, g, n_q=0, ws_bytes=big) == "KVMEM_ERR_SHAPE"
     assert _attn(L, g, n_pages=0, ws_bytes=big) == "KVMEM_ERR_SHAPE"
     assert _attn(L, g1(head_dim=80), ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"
+
+
+@no_gpu
+def test_rope_calls_validation(L):
+    g = ctypes.byref(g1())
+    # index from encoded keys
+    assert _status(L.kvmem_build_index_rope(g, FAKE, 10, FAKE, None, 0.5, 0, 4, FAKE, None)) == "KVMEM_ERR_SHAPE"
+    assert _status(L.kvmem_build_index_rope(g, FAKE, 10, FAKE, None, float("inf"), 0, 4, FAKE, None)) \
+        == "KVMEM_ERR_SHAPE"
+    assert _status(L.kvmem_build_index_rope(g, None, 10, FAKE, None, 1e6, 0, 4, FAKE, None)) == "KVMEM_ERR_NULL"
+    assert _status(L.kvmem_build_index_rope(g, FAKE, 10, FAKE, MISALIGNED, 1e6, 0, 4, FAKE, None)) \
+        == "KVMEM_ERR_ALIGN"
+    assert _status(L.kvmem_build_index_rope(g, None, 10, None, None, 1e6, 0, 0, None, None)) == "KVMEM_OK"
+    # materialisation
+    m = lambda **kw: _status(L.kvmem_materialize(
+        g, kw.get("base", 1e6), kw.get("raw", FAKE), FAKE, kw.get("nsrc", 10), FAKE, kw.get("pos", FAKE), FAKE,
+        kw.get("n", 4), FAKE, FAKE, kw.get("ndst", 10), None))
+    assert m(base=1.0) == "KVMEM_ERR_SHAPE"
+    assert m(raw=None) == "KVMEM_ERR_NULL"
+    assert m(pos=None) == "KVMEM_ERR_NULL"
+    assert m(nsrc=0) == "KVMEM_ERR_SHAPE"
+    assert m(ndst=-1) == "KVMEM_ERR_SHAPE"
+    assert m(n=-1) == "KVMEM_ERR_SHAPE"
+    assert m(pos=MISALIGNED) == "KVMEM_ERR_ALIGN"
+    assert m(n=0, raw=None, pos=None) == "KVMEM_OK"
+    # delta re-encoding
+    r = lambda **kw: _status(L.kvmem_rerope(g, kw.get("base", 1e6), kw.get("k", FAKE), kw.get("np", 10),
+                                            kw.get("pages", FAKE), FAKE, kw.get("n", 4), None))
+    assert r(base=float("nan")) == "KVMEM_ERR_SHAPE"
+    assert r(k=None) == "KVMEM_ERR_NULL"
+    assert r(np=0) == "KVMEM_ERR_SHAPE"
+    assert r(pages=MISALIGNED) == "KVMEM_ERR_ALIGN"
+    assert r(n=0, k=None, pages=None) == "KVMEM_OK"
+    bad = g1(head_dim=96)
+    assert _status(L.kvmem_rerope(ctypes.byref(bad), 1e6, FAKE, 10, FAKE, FAKE, 4, None)) == "KVMEM_ERR_UNSUPPORTED"
