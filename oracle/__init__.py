@@ -14,6 +14,9 @@ Entry points and the passages they follow:
   view_attention    Sec. 4.4 / Sec. 5.3: attention through the view's page table
   masked_dense_attention   the same attention as dense attention with the
                     non-view blocks masked out
+  decode_e4m3, decode_fp8  FP8 K/V (the KV-cache precision of Sec. 6's
+                    platforms): OCP E4M3 codes to fp64, times the pool's scale;
+                    the entry points above take the decoded pool as float64
 """
 import ctypes
 import os
@@ -71,13 +74,36 @@ def _c(a, dtype):
 
 
 def _pool(pool):
-    """A K/V pool is float32 or bf16 stored as raw uint16 bits."""
+    """A K/V pool is float32, bf16 stored as raw uint16 bits, or float64 (an
+    FP8 pool decoded by decode_fp8)."""
     pool = np.ascontiguousarray(pool)
     if pool.dtype == np.float32:
         return pool, 0
     if pool.dtype == np.uint16:
         return pool, 1
-    raise TypeError("pool must be float32 or uint16 (bf16 bits)")
+    if pool.dtype == np.float64:
+        return pool, 2
+    raise TypeError("pool must be float32, uint16 (bf16 bits) or float64")
+
+
+def decode_e4m3(codes):
+    """OCP FP8 E4M3 (the FN variant: 1 sign, 4 exponent bits with bias 7, 3
+    mantissa bits, no infinities; S.1111.111 is NaN) to fp64:
+      exponent field e > 0: (-1)^s * 2^(e-7) * (1 + m/8)
+      exponent field 0:     (-1)^s * 2^(-6) * (m/8)"""
+    c = np.asarray(codes, np.uint8).astype(np.int64)
+    s = np.where(c >> 7, -1.0, 1.0)
+    e = (c >> 3) & 15
+    m = (c & 7).astype(np.float64)
+    val = np.where(e > 0, np.ldexp(1.0 + m / 8.0, e - 7), np.ldexp(m / 8.0, -6))
+    val = s * val
+    return np.where((c & 0x7F) == 0x7F, np.nan, val)
+
+
+def decode_fp8(codes, scale):
+    """An FP8 K/V pool (E4M3 codes with one fp32 scale per pool) as fp64 values:
+    decode_e4m3(code) * scale."""
+    return decode_e4m3(codes) * float(np.float32(scale))
 
 
 def _check(rc, what):

@@ -28,15 +28,18 @@ int oracle_num_threads(void) {
 #endif
 }
 
-/* Widen one stored K/V element to fp64.  A bf16 value is the top half of the
- * fp32 with the same bits, so the widening is exact. */
-static double load_elem(const void *pool, int kv_is_bf16, int64_t i) {
-    if (kv_is_bf16) {
+/* Widen one stored K/V element to fp64 (pool element type: 0 fp32, 1 bf16
+ * bits, 2 fp64).  A bf16 value is the top half of the fp32 with the same
+ * bits, so every widening is exact.  (FP8 pools reach the oracle decoded to
+ * fp64, see the Python wrapper.) */
+static double load_elem(const void *pool, int kv_type, int64_t i) {
+    if (kv_type == 1) {
         uint32_t bits = (uint32_t)((const uint16_t *)pool)[i] << 16;
         float f;
         memcpy(&f, &bits, sizeof f);
         return (double)f;
     }
+    if (kv_type == 2) return ((const double *)pool)[i];
     return (double)((const float *)pool)[i];
 }
 
@@ -47,7 +50,7 @@ static int64_t pool_offset(int64_t page, int g, int t, int j, int n_kv_heads, in
 }
 
 /* ---- Eq. 9: Mean-K block summary ------------------------------------- */
-int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_type,
                   const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                   int32_t first_block, int32_t n_blocks, float *index) {
     if (!k_pool || !block_to_page || !index || n_kv_heads <= 0 || block_tokens <= 0 ||
@@ -65,7 +68,7 @@ int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16
             for (int j = 0; j < head_dim; ++j) {
                 double sum = 0.0;
                 for (int t = 0; t < block_tokens; ++t)
-                    sum += load_elem(k_pool, kv_is_bf16,
+                    sum += load_elem(k_pool, kv_type,
                                      pool_offset(page, g, t, j, n_kv_heads, block_tokens, head_dim));
                 double mean = sum / (double)block_tokens;
                 index[((int64_t)b * n_kv_heads + g) * head_dim + j] = (float)mean;
@@ -108,7 +111,7 @@ int oracle_rope(int64_t n_rows, int head_dim, const double *x, const int64_t *po
     return 0;
 }
 
-int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_type,
                        const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                        const int64_t *block_pos, double base, int32_t first_block, int32_t n_blocks,
                        float *index) {
@@ -133,7 +136,7 @@ int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_is
                 for (int t = 0; t < block_tokens; ++t) {
                     /* the stored key carries RoPE at p0 + t: rotate it back */
                     for (int j = 0; j < head_dim; ++j)
-                        row[j] = load_elem(k_pool, kv_is_bf16,
+                        row[j] = load_elem(k_pool, kv_type,
                                            pool_offset(page, g, t, j, n_kv_heads, block_tokens, head_dim));
                     rope_row(row, -(p0 + t), head_dim, base);
                     for (int j = 0; j < head_dim; ++j) sum[j] += row[j];
@@ -306,7 +309,7 @@ int oracle_select(int n_sel, const double *relevance, int32_t n_blocks, int32_t 
  * offset of that token's value row.  out = sum_t softmax(a)_t V_t,
  * lse = log sum_t exp(a_t). */
 static void attend(int64_t n_tok, const double *a, const int64_t *v_row, const void *v_pool,
-                   int kv_is_bf16, int head_dim, double *out, double *lse) {
+                   int kv_type, int head_dim, double *out, double *lse) {
     double mx = -INFINITY;
     for (int64_t t = 0; t < n_tok; ++t)
         if (a[t] > mx) mx = a[t];
@@ -315,14 +318,14 @@ static void attend(int64_t n_tok, const double *a, const int64_t *v_row, const v
     for (int64_t t = 0; t < n_tok; ++t) {
         double w = exp(a[t] - mx); /* exp(-inf) = 0 for masked tokens */
         z += w;
-        for (int j = 0; j < head_dim; ++j) out[j] += w * load_elem(v_pool, kv_is_bf16, v_row[t] + j);
+        for (int j = 0; j < head_dim; ++j) out[j] += w * load_elem(v_pool, kv_type, v_row[t] + j);
     }
     for (int j = 0; j < head_dim; ++j) out[j] /= z;
     *lse = mx + log(z);
 }
 
 int oracle_view_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
-                          int block_tokens, int kv_is_bf16, const float *q,
+                          int block_tokens, int kv_type, const float *q,
                           const void *k_pool, const void *v_pool, int64_t n_pages,
                           const int32_t *view_pages, int n_sel, int32_t n_view,
                           int32_t last_page_tokens, double scale, double *out, double *lse) {
@@ -359,12 +362,12 @@ int oracle_view_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
                 int64_t base = pool_offset(page, g, t, 0, n_kv_heads, block_tokens, head_dim);
                 double dot = 0.0;
                 for (int j = 0; j < head_dim; ++j)
-                    dot += (double)qv[j] * load_elem(k_pool, kv_is_bf16, base + j);
+                    dot += (double)qv[j] * load_elem(k_pool, kv_type, base + j);
                 a[t_out] = scale * dot;
                 v_row[t_out] = base;
             }
         }
-        attend(n_tok, a, v_row, v_pool, kv_is_bf16, head_dim, out + (int64_t)row * head_dim,
+        attend(n_tok, a, v_row, v_pool, kv_type, head_dim, out + (int64_t)row * head_dim,
                lse + row);
         free(a);
         free(v_row);
@@ -373,7 +376,7 @@ int oracle_view_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
 }
 
 int oracle_masked_dense_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
-                                  int block_tokens, int kv_is_bf16, const float *q,
+                                  int block_tokens, int kv_type, const float *q,
                                   const void *k_pool, const void *v_pool, int64_t n_pages,
                                   const int32_t *block_to_page, int32_t n_blocks,
                                   const int32_t *view_blocks, int n_sel, int32_t n_view,
@@ -419,12 +422,12 @@ int oracle_masked_dense_attention(int n_q, int n_q_heads, int n_kv_heads, int he
                 int64_t base = pool_offset(page, g, t, 0, n_kv_heads, block_tokens, head_dim);
                 double dot = 0.0;
                 for (int j = 0; j < head_dim; ++j)
-                    dot += (double)qv[j] * load_elem(k_pool, kv_is_bf16, base + j);
+                    dot += (double)qv[j] * load_elem(k_pool, kv_type, base + j);
                 a[ti] = keep ? scale * dot : -INFINITY;
                 v_row[ti] = base;
             }
         }
-        attend(n_tok, a, v_row, v_pool, kv_is_bf16, head_dim, out + (int64_t)row * head_dim,
+        attend(n_tok, a, v_row, v_pool, kv_type, head_dim, out + (int64_t)row * head_dim,
                lse + row);
         free(in_view);
         free(a);

@@ -8,7 +8,8 @@
  *
  * Paper: "KVMem" (arXiv 2609.04852).  Every entry point cites the passage of
  * the paper it follows.  Layouts (all row-major, C order):
- *   K/V page pool   [n_pages][n_kv_heads][block_tokens][head_dim]  (f32 or bf16 bits)
+ *   K/V page pool   [n_pages][n_kv_heads][block_tokens][head_dim]  element type kv_type:
+ *                   0 fp32, 1 bf16 bits, 2 fp64
  *   Mean-K index    [n_layers][n_blocks][n_kv_heads][head_dim]      float
  *   query           [n_layers][n_q][n_q_heads][head_dim]            float
  *   relevance       [n_sel][n_blocks]                                double
@@ -42,7 +43,7 @@ extern "C" {
  * divide by block_tokens in fp64, round once to fp32.  Rows
  * [first_block, first_block + n_blocks) of `index` ([*][Hkv][d]) are written;
  * block b reads page block_to_page[b] of k_pool. */
-int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+int oracle_mean_k(int n_kv_heads, int block_tokens, int head_dim, int kv_type,
                   const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                   int32_t first_block, int32_t n_blocks, float *index);
 
@@ -65,7 +66,7 @@ int oracle_rope(int64_t n_rows, int head_dim, const double *x, const int64_t *po
  * block's original frame b * block_tokens + t), is rotated back to position
  * 0 in fp64, and the block's mean is rounded once to fp32 (index layout as
  * oracle_mean_k). */
-int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_is_bf16,
+int oracle_mean_k_rope(int n_kv_heads, int block_tokens, int head_dim, int kv_type,
                        const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                        const int64_t *block_pos, double base, int32_t first_block, int32_t n_blocks,
                        float *index);
@@ -109,7 +110,7 @@ int oracle_select(int n_sel, const double *relevance, int32_t n_blocks, int32_t 
  * out[m][h] = sum_t softmax(a)_t V[page][g][t], lse[m][h] = log sum_t exp(a_t).
  * q is one layer: [n_q][Hq][d].  Outputs are fp64. */
 int oracle_view_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
-                          int block_tokens, int kv_is_bf16, const float *q,
+                          int block_tokens, int kv_type, const float *q,
                           const void *k_pool, const void *v_pool, int64_t n_pages,
                           const int32_t *view_pages, int n_sel, int32_t n_view,
                           int32_t last_page_tokens, double scale, double *out, double *lse);
@@ -120,7 +121,7 @@ int oracle_view_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
  * appear in view_blocks[s].  The final view block (view_blocks[s][n_view-1])
  * keeps only last_page_tokens tokens.  Outputs are fp64. */
 int oracle_masked_dense_attention(int n_q, int n_q_heads, int n_kv_heads, int head_dim,
-                                  int block_tokens, int kv_is_bf16, const float *q,
+                                  int block_tokens, int kv_type, const float *q,
                                   const void *k_pool, const void *v_pool, int64_t n_pages,
                                   const int32_t *block_to_page, int32_t n_blocks,
                                   const int32_t *view_blocks, int n_sel, int32_t n_view,

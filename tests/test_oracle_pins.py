@@ -499,3 +499,77 @@ class TestRope:
         lhs = oracle.rope(q, P, 1e6) @ k_out[2, 1, 9]
         rhs = q @ oracle.rope(raw[src[2], 1, 9], (pos[2] + 9) - P, 1e6)
         assert abs(lhs - rhs) < 1e-9
+
+
+# ---- FP8 K/V (the KV-cache precision of the evaluation platforms, Sec. 6):
+# OCP E4M3 codes with one fp32 scale per pool ------------------------------
+def fp8_pools(seed, p, hkv, bt, d, scale):
+    """E4M3 codes of two pools (quantised by torch's own float8 cast) and their
+    fp64 values decoded by torch."""
+    g = rng(seed)
+    out = []
+    for _ in range(2):
+        x = torch.from_numpy((g.standard_normal((p, hkv, bt, d)) * 3.0 / scale).astype(np.float32))
+        codes = x.clamp(-448.0, 448.0).to(torch.float8_e4m3fn)
+        out.append((codes.view(torch.uint8).numpy(), codes.to(torch.float64).numpy() * float(np.float32(scale))))
+    return out
+
+
+class TestFp8:
+    def test_decode_matches_torch_float8_e4m3fn(self):
+        codes = np.arange(256, dtype=np.uint8)
+        ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+        got = oracle.decode_e4m3(codes)
+        np.testing.assert_array_equal(got, ref)
+        assert np.array_equal(np.signbit(got[~np.isnan(got)]), np.signbit(ref[~np.isnan(ref)]))
+
+    def test_format_landmarks(self):
+        d = oracle.decode_e4m3(np.arange(256, dtype=np.uint8))
+        assert d[0x38] == 1.0 and d[0xB8] == -1.0
+        assert d[0x7E] == 448.0 and d[0xFE] == -448.0       # largest finite
+        assert d[0x08] == 2.0 ** -6                          # smallest normal
+        assert d[0x01] == 2.0 ** -9                          # smallest subnormal
+        assert d[0x07] == 7 * 2.0 ** -9                      # largest subnormal
+        assert d[0x00] == 0.0 and np.signbit(d[0x80])       # +0, -0
+        assert np.isnan(d[0x7F]) and np.isnan(d[0xFF])       # the only NaNs, no infinities
+        assert np.isfinite(np.delete(d, [0x7F, 0xFF])).all()
+
+    def test_positive_codes_are_ordered_and_sign_is_the_top_bit(self):
+        d = oracle.decode_e4m3(np.arange(256, dtype=np.uint8))
+        assert (np.diff(d[:0x7F]) > 0).all()
+        np.testing.assert_array_equal(d[0x80:0xFF], -d[:0x7F])
+        # eight codes per binade, each binade twice as wide as the one below
+        for e in range(2, 16):
+            assert d[8 * e] == 2 * d[8 * (e - 1)]
+
+    def test_pool_scale_multiplies(self):
+        codes = np.arange(256, dtype=np.uint8)
+        s = np.float32(0.0173)
+        np.testing.assert_array_equal(oracle.decode_fp8(codes, s), oracle.decode_e4m3(codes) * float(s))
+
+    @pytest.mark.parametrize("bt", [16, 5])
+    def test_mean_k_of_fp8_pool_is_exact_mean(self, bt):
+        s = np.float32(0.0173)
+        (codes, vals), _ = fp8_pools(40 + bt, 4, 2, bt, 8, s)
+        b2p = np.array([2, 0, 3, 1], np.int32)
+        idx = oracle.mean_k(oracle.decode_fp8(codes, s), b2p)
+        for b in range(4):
+            for g in range(2):
+                for j in range(8):
+                    exact = sum(Fraction(float(x)) for x in vals[b2p[b], g, :, j]) / bt
+                    assert idx[b, g, j] == round_to_f32(exact)
+
+    def test_attention_on_fp8_pool_matches_torch_sdpa(self):
+        p, hkv, bt, d, hq = 20, 2, 16, 32, 4
+        (kc, kv), (vc, vv) = fp8_pools(50, p, hkv, bt, d, np.float32(2.0 ** -5))
+        q = rng(51).standard_normal((1, hq, d)).astype(np.float32)
+        pages = rng(52).choice(p, 7, replace=False).astype(np.int32)[None]
+        out, lse = oracle.view_attention(q, oracle.decode_fp8(kc, 2.0 ** -5), oracle.decode_fp8(vc, 2.0 ** -5),
+                                         pages, last_page_tokens=9, scale=0.2)
+        for h in range(hq):
+            g = h // (hq // hkv)
+            kk = np.concatenate([kv[pg, g] for pg in pages[0]], 0)[:-(bt - 9)]
+            vv_ = np.concatenate([vv[pg, g] for pg in pages[0]], 0)[:-(bt - 9)]
+            o_ref, l_ref = sdpa(q[0, h][None], kk[None], vv_[None], 0.2)
+            np.testing.assert_allclose(out[0, h], o_ref[0], rtol=0, atol=1e-12)
+            assert lse[0, h] == pytest.approx(float(l_ref[0]), abs=1e-12)
