@@ -79,11 +79,33 @@ def algorithmic_bytes(cfg):
 
 
 def cpu_oracle_baseline(w, seconds):
-    """fp64 oracle on the same workload: relevance + selection + attention per step."""
+    """fp64 oracle on the same workload: relevance + selection + attention per step.
+    FP8 pools are decoded by the oracle's decoder: for the index in chunks of
+    blocks beforehand, and inside every timed step for the view's pages."""
     import oracle
     cfg = w.cfg
     mode = oracle.MEAN_ALL if cfg.mode == "mean_all" else oracle.MAX_GROUP
-    index = [oracle.mean_k(w.k_pool[l], w.block_to_page) for l in range(len(w.k_pool))]
+    fp8 = cfg.kv_dtype == "fp8"
+
+    def index_of(pool):
+        if not fp8:
+            return oracle.mean_k(pool, w.block_to_page)
+        rows = []
+        for b0 in range(0, cfg.n_blocks, 4096):
+            pages = w.block_to_page[b0:b0 + 4096]
+            sub = oracle.decode_fp8(pool[pages], cfg.kv_scale)
+            rows.append(oracle.mean_k(sub, np.arange(len(pages), dtype=np.int32)))
+        return np.concatenate(rows, 0)
+
+    def attend(q, kp, vp_pool, vp):
+        if not fp8:
+            return oracle.view_attention(q, kp, vp_pool, vp)
+        pages, local = np.unique(vp, return_inverse=True)
+        local = local.reshape(vp.shape).astype(np.int32)
+        return oracle.view_attention(q, oracle.decode_fp8(kp[pages], cfg.kv_scale),
+                                     oracle.decode_fp8(vp_pool[pages], cfg.kv_scale), local)
+
+    index = [index_of(w.k_pool[l]) for l in range(len(w.k_pool))]
     n = 0
     t0 = time.perf_counter()
     while True:
@@ -93,7 +115,7 @@ def cpu_oracle_baseline(w, seconds):
             k = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, cfg.block_tokens, cfg.n_blocks,
                              cfg.sink_blocks, cfg.n_recent)
             _, vp = oracle.select(rel, cfg.sink_blocks, cfg.n_recent, k, w.block_to_page)
-            oracle.view_attention(qs[l], w.k_pool[l], w.v_pool[l], vp)
+            attend(qs[l], w.k_pool[l], w.v_pool[l], vp)
         n += 1
         el = time.perf_counter() - t0
         if el >= seconds or n >= 50:
@@ -244,8 +266,10 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
 
-    mat_ms = timed(lambda: K.kvmem_materialize(st.geom, rope_base, st.k_pool, st.v_pool, src, cpos, dst, kx, vx))
-    rer_ms = timed(lambda: K.kvmem_rerope(st.geom, rope_base, kx, dst, shift))
+    fp8 = cfg.kv_dtype == "fp8"  # FP8 pools are not re-encoded (that would quantise K again)
+    mat_ms = None if fp8 else timed(
+        lambda: K.kvmem_materialize(st.geom, rope_base, st.k_pool, st.v_pool, src, cpos, dst, kx, vx))
+    rer_ms = None if fp8 else timed(lambda: K.kvmem_rerope(st.geom, rope_base, kx, dst, shift))
     irope_ms = timed(lambda: K.kvmem_build_index_rope(st.geom, st.k_pool, st.block_to_page, 0, cfg.n_blocks,
                                                       st.index, rope_base), reps=3)
     st.build_index()  # restore the position-independent index
@@ -253,13 +277,15 @@ def main():
     mat_bytes = 4 * n_view * page_bytes  # read K and V, write K and V
     rer_bytes = 2 * n_view * page_bytes  # read and write K
     irope_bytes = build_bytes // cfg.n_layers
+    def rate(ms, nbytes):
+        if ms is None:
+            return "not applicable to FP8 pools"
+        return {"ms": round(ms, 4), "bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                "frac_of_peak": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+
     position = {"view_blocks": n_view,
-                "materialize": {"ms": round(mat_ms, 4), "bytes": mat_bytes,
-                                "GBps": round(mat_bytes / (mat_ms * 1e-3) / 1e9, 1),
-                                "frac_of_peak": round(mat_bytes / (mat_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
-                "rerope": {"ms": round(rer_ms, 4), "bytes": rer_bytes,
-                           "GBps": round(rer_bytes / (rer_ms * 1e-3) / 1e9, 1),
-                           "frac_of_peak": round(rer_bytes / (rer_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+                "materialize": rate(mat_ms, mat_bytes),
+                "rerope": rate(rer_ms, rer_bytes),
                 "index_from_encoded_keys": {"ms": round(irope_ms, 4), "bytes": irope_bytes,
                                             "GBps": round(irope_bytes / (irope_ms * 1e-3) / 1e9, 1)}}
     del kx, vx

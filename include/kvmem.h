@@ -29,7 +29,9 @@
  *
  * Layouts.  Hkv = n_kv_heads, Hq = n_q_heads (a multiple of Hkv, G = Hq/Hkv),
  * d = head_dim, Bt = block_tokens (one history block occupies one page):
- *   K/V page pool  [n_pages][Hkv][Bt][d]      kv_dtype (f32, or bf16 bits)
+ *   K/V page pool  [n_pages][Hkv][Bt][d]      kv_dtype (f32, bf16 bits, or FP8
+ *                  E4M3 codes, one byte each, read as code value * k_scale
+ *                  for K and * v_scale for V)
  *   Mean-K index   [n_layers][T][Hkv][d/4][64][4]  float, tiled: T = ceil(M/64)
  *                  tiles of 64 blocks, M = history blocks; the entry of block
  *                  b, KV head g, dimension j is at
@@ -77,7 +79,11 @@ typedef enum {
     KVMEM_ERR_HIP = -8          /* a HIP runtime call or kernel launch failed */
 } kvmem_status;
 
-typedef enum { KVMEM_F32 = 0, KVMEM_BF16 = 1 } kvmem_dtype;
+/* Element type of the K/V pools.  KVMEM_FP8_E4M3 is the OCP 8-bit float with
+ * 4 exponent bits (bias 7) and 3 mantissa bits, no infinities and NaN at
+ * S.1111.111 (the FP8 KV cache of the paper's evaluation platforms, Sec. 6);
+ * each pool carries one fp32 scale (kvmem_geom.k_scale, .v_scale). */
+typedef enum { KVMEM_F32 = 0, KVMEM_BF16 = 1, KVMEM_FP8_E4M3 = 2 } kvmem_dtype;
 
 /* How Eq. 10's per-(layer, query token, query head) block softmaxes are
  * combined into selection scores. */
@@ -99,6 +105,9 @@ typedef struct {
     int32_t head_dim;     /* d */
     int32_t block_tokens; /* Bt, tokens per block and per page (Sec. 3.1, Sec. 5.2) */
     int32_t kv_dtype;     /* kvmem_dtype of the K/V pools */
+    float k_scale;        /* KVMEM_FP8_E4M3: K element = decoded code * k_scale (finite, > 0);
+                             ignored for the other types */
+    float v_scale;        /* KVMEM_FP8_E4M3: V element = decoded code * v_scale (finite, > 0) */
 } kvmem_geom;
 
 /* Bytes of one layer's Mean-K index for n_blocks history blocks (the tiled
@@ -111,7 +120,8 @@ size_t kvmem_index_bytes(const kvmem_geom *geom, int32_t n_blocks);
  * For every block b in [first_block, first_block + n_blocks) and KV head g:
  *   index[b][g][j] = (1/Bt) * sum_{t < Bt} K[block_to_page[b]][g][t][j],
  * summed exactly (fp64) and rounded once to fp32, so the result does not depend
- * on summation order.  Keys are taken as position independent (any RoPE already
+ * on summation order (FP8 pools: the decoded codes are summed exactly, and the
+ * sum times k_scale / Bt is rounded once).  Keys are taken as position independent (any RoPE already
  * removed by the caller).  Call it once per layer, with that layer's pool and
  * index; it only writes the rows of the given range, so completed blocks can be
  * indexed incrementally while their keys are resident.
@@ -173,7 +183,9 @@ kvmem_status kvmem_materialize(const kvmem_geom *geom, double rope_base, const v
  * K (kvmem_materialize), which is the caller's policy.
  *   k_pool           dev [n_pages][Hkv][Bt][d] kv_dtype, updated in place
  *   pages            dev [n_list] int32 (distinct); delta_positions dev [n_list] int64
- * Pages outside the pool are skipped. */
+ * Pages outside the pool are skipped.  kvmem_materialize and kvmem_rerope take
+ * f32 and bf16 pools; FP8 pools return KVMEM_ERR_UNSUPPORTED (re-encoding would
+ * quantise K again). */
 kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool, int64_t n_pages,
                           const int32_t *pages, const int64_t *delta_positions, int32_t n_list, void *stream);
 
@@ -248,7 +260,8 @@ size_t kvmem_sparse_attn_workspace_bytes(const kvmem_geom *geom, int32_t n_q_tok
  * same view (no mask among them).
  *
  *   q              dev  float [n_q][Hq][d]   one layer
- *   k_pool, v_pool dev  [n_pages][Hkv][Bt][d] kv_dtype
+ *   k_pool, v_pool dev  [n_pages][Hkv][Bt][d] kv_dtype (FP8: K_t and V_t are
+ *                       the decoded codes times k_scale and v_scale)
  *   view_pages     dev  int32 [n_sel][n_view], n_sel = 1 or Hkv
  *   last_page_tokens    1 .. Bt
  *   scale               <= 0 selects 1/sqrt(d)

@@ -445,6 +445,12 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
 //           tokens is the same permutation on both sides.
 // Waves take the split's 32-token tiles in turn and are merged in LDS; one
 // partial (O, max, sum) per row is written in the format attn_combine reads.
+// FP8 K/V (E4M3 codes): every code is exactly a bf16 value, so the same MFMA
+// products run on codes widened in registers (v_cvt_scalef32_pk_bf16_fp8, two
+// codes per instruction); k_scale is folded into Q and v_scale into the
+// partial output.  One 16-byte K load then holds 16 dims, which feed two
+// 32-long contractions: chunk 2c+u takes dims 64c + 16kg + 8u + [0, 8), and Q
+// is laid out the same way.  V codes are widened before they go to LDS.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kMfmaRows = 16;
@@ -469,17 +475,35 @@ __device__ inline void split_bf16x8(const float (&x)[8], bf16x8_t &hi, bf16x8_t 
 
 __device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-template <int D, int BT>
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// 4 E4M3 codes -> 4 bf16 (exact), as two dwords of bf16 pairs in code order
+__device__ inline uint2 fp8x4_to_bf16x4(uint32_t w) {
+    return make_uint2(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false)),
+                      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true)));
+}
+// 8 codes (two dwords) -> one bf16x8 operand
+__device__ inline bf16x8_t fp8x8_to_bf16x8(uint32_t w0, uint32_t w1) {
+    const uint2 a = fp8x4_to_bf16x4(w0), b = fp8x4_to_bf16x4(w1);
+    return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// T = uint16_t (bf16 bits) or uint8_t (FP8 E4M3 codes)
+template <typename T, int D, int BT>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
-    const float *__restrict__ q, const uint16_t *__restrict__ k_pool, const uint16_t *__restrict__ v_pool,
+    const float *__restrict__ q, const T *__restrict__ k_pool, const T *__restrict__ v_pool,
     int64_t n_pages, const int32_t *__restrict__ view_pages, int n_sel, int n_view, int last_page_tokens,
     int n_kv_heads, int n_q_heads, int group, int rows_total, int pages_per_split, int n_splits,
-    float qscale, float *__restrict__ part) {
+    float qscale, float v_scale, float *__restrict__ part) {
+    constexpr bool F8 = sizeof(T) == 1;
+    constexpr int EPL = 16 / sizeof(T);  // elements per 16-byte load
     constexpr int KC = D / 32;           // 32-long chunks of the head dimension (scores)
+    constexpr int KL = F8 ? KC / 2 : KC; // 16-byte K loads per lane per 16-token half
     constexpr int MB = D / 16;           // 16-dim blocks of the output
     constexpr int VP = D + 4;            // LDS row pitch of the V tile, in halves
-    constexpr int VL = kMfmaTile * D / 8 / kWave;  // 16-byte V loads per lane per tile
-    static_assert(VL * kWave * 8 == kMfmaTile * D, "V tile split over the wave");
+    constexpr int VL = kMfmaTile * D / EPL / kWave;  // 16-byte V loads per lane per tile
+    static_assert(VL * kWave * EPL == kMfmaTile * D, "V tile split over the wave");
+    // first dim of the lane's 8-long slice of contraction chunk c (Q and K alike)
+    auto chunk_dim = [&](int c, int kg) { return F8 ? 64 * (c / 2) + 16 * kg + 8 * (c % 2) : 32 * c + 8 * kg; };
     __shared__ uint16_t sm_v[kAttnWaves][kMfmaTile * VP];
     __shared__ float sm_m[kAttnWaves][kMfmaRows], sm_l[kAttnWaves][kMfmaRows];
     __shared__ int sm_bad[kAttnWaves];
@@ -507,17 +531,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     __syncthreads();
     const bool any_bad = sm_bad[0] != 0;
 
-    // Q^T operand: lane holds q[row r16][32c + 8kg + j] * qscale as hi + lo
+    // Q^T operand: lane holds q[row r16][chunk_dim(c, kg) + j] * qscale as hi + lo
     // (rows past rows_total pad the 16-row tile with zeros and are not written)
     bf16x8_t qhi[KC], qlo[KC];
     {
         const int row = min(row0 + r16, rows_total - 1), m = row / group, hh = row % group;
         const float qs = row0 + r16 < rows_total ? qscale : 0.f;
-        const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D + 8 * kg;
+        const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D;
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
-            const float4 a = *reinterpret_cast<const float4 *>(qp + 32 * c);
-            const float4 b = *reinterpret_cast<const float4 *>(qp + 32 * c + 4);
+            const float4 a = *reinterpret_cast<const float4 *>(qp + chunk_dim(c, kg));
+            const float4 b = *reinterpret_cast<const float4 *>(qp + chunk_dim(c, kg) + 4);
             const float x[8] = {a.x * qs, a.y * qs, a.z * qs, a.w * qs, b.x * qs, b.y * qs, b.z * qs, b.w * qs};
             split_bf16x8(x, qhi[c], qlo[c]);
         }
@@ -528,12 +552,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     float mrun = -INFINITY, lpart = 0.f;
 
     // K and V of tile t (16 tokens of a half never cross a page): K half h,
-    // lane -> token 16h + r16, dims 32c + 8kg ..; V load i -> token
-    // (lane + 64 i) / (D/8), 16 bytes at dim 8 * ((lane + 64 i) % (D/8)).
-    // Tokens past the split read token 0 of the split's first page (in bounds)
-    // and are masked out of the softmax.
-    auto load_tile = [&](int t, uint4 (&kb)[2][KC], uint4 (&vb)[VL]) {
-        const uint16_t *kbase[2], *vbase[2];
+    // lane -> token 16h + r16, 16 bytes at dim chunk_dim(c * EPL / 8, kg); V
+    // load i -> token (lane + 64 i) / (D/EPL), 16 bytes at dim
+    // EPL * ((lane + 64 i) % (D/EPL)).  Tokens past the split read the split's
+    // last token again (in bounds) and are masked out of the softmax.
+    auto load_tile = [&](int t, uint4 (&kb)[2][KL], uint4 (&vb)[VL]) {
+        const T *kbase[2], *vbase[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int s0 = min(t * kMfmaTile + 16 * h, n_tok - 1);
@@ -546,29 +570,36 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         for (int h = 0; h < 2; ++h) {
             const int tok = min(16 * h + r16, n_tok - 1 - (t * kMfmaTile + 16 * h) + 16 * h);
 #pragma unroll
-            for (int c = 0; c < KC; ++c)
-                kb[h][c] = load_stream16(kbase[h] + (int64_t)(tok - 16 * h) * D + 32 * c + 8 * kg);
+            for (int c = 0; c < KL; ++c)
+                kb[h][c] = load_stream16(kbase[h] + (int64_t)(tok - 16 * h) * D + chunk_dim(c * EPL / 8, kg));
         }
 #pragma unroll
         for (int i = 0; i < VL; ++i) {
-            const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
+            const int idx = lane + kWave * i, x = idx / (D / EPL), ch = idx % (D / EPL);
             const int h = x / 16;
             const int tok = min(x, n_tok - 1 - t * kMfmaTile);
-            vb[i] = load_stream16(vbase[h] + (int64_t)(tok - 16 * h) * D + 8 * ch);
+            vb[i] = load_stream16(vbase[h] + (int64_t)(tok - 16 * h) * D + EPL * ch);
         }
     };
     uint16_t *my_v = sm_v[wave];
-    // V tile to LDS (row x, 8 halves at 8ch); a wave reads only its own tile
+    // V tile to LDS as bf16 (row x, EPL values at EPL*ch); a wave reads only its own tile
     auto stage_v = [&](const uint4 (&vb)[VL]) {
 #pragma unroll
         for (int i = 0; i < VL; ++i) {
-            const int idx = lane + kWave * i, x = idx / (D / 8), ch = idx % (D / 8);
-            uint2 *dst = reinterpret_cast<uint2 *>(my_v + x * VP + 8 * ch);
-            dst[0] = make_uint2(vb[i].x, vb[i].y);
-            dst[1] = make_uint2(vb[i].z, vb[i].w);
+            const int idx = lane + kWave * i, x = idx / (D / EPL), ch = idx % (D / EPL);
+            uint2 *dst = reinterpret_cast<uint2 *>(my_v + x * VP + EPL * ch);
+            if constexpr (F8) {
+                dst[0] = fp8x4_to_bf16x4(vb[i].x);
+                dst[1] = fp8x4_to_bf16x4(vb[i].y);
+                dst[2] = fp8x4_to_bf16x4(vb[i].z);
+                dst[3] = fp8x4_to_bf16x4(vb[i].w);
+            } else {
+                dst[0] = make_uint2(vb[i].x, vb[i].y);
+                dst[1] = make_uint2(vb[i].z, vb[i].w);
+            }
         }
     };
-    auto process = [&](int t, const uint4 (&kb)[2][KC]) {
+    auto process = [&](int t, const uint4 (&kb)[2][KL]) {
         // scores of the 32 tokens: lane gets row r16, tokens 16h + 4kg + i
         float sc[8];
 #pragma unroll
@@ -576,7 +607,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             f32x4_t st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < KC; ++c) {
-                const bf16x8_t kk = as_bf16x8(kb[h][c]);
+                bf16x8_t kk;
+                if constexpr (F8) {
+                    const uint4 w = kb[h][c / 2];
+                    kk = c % 2 == 0 ? fp8x8_to_bf16x8(w.x, w.y) : fp8x8_to_bf16x8(w.z, w.w);
+                } else {
+                    kk = as_bf16x8(kb[h][c]);
+                }
                 st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qhi[c], st, 0, 0, 0);
                 st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qlo[c], st, 0, 0, 0);
             }
@@ -626,7 +663,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     // while the current one is processed (its V goes to LDS first, so only
     // one V tile is held in registers)
     {
-        uint4 ka[2][KC], kb2[2][KC], vx[VL];
+        uint4 ka[2][KL], kb2[2][KL], vx[VL];
         int t = wave;
         if (t < n_tiles) load_tile(t, ka, vx);
         while (t < n_tiles) {
@@ -673,7 +710,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             l += sm_l[w][r] * f;
         }
         float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r) * (D + kPartStride);
-        dst[d] = any_bad ? __builtin_nanf("") : o;
+        dst[d] = any_bad ? __builtin_nanf("") : o * v_scale;
         if (d == 0) {
             dst[D] = mx;
             dst[D + 1] = l;
@@ -773,15 +810,15 @@ hipError_t launch_row16(const AttnPlan &p, const float *q, const void *k_pool, c
     return hipGetLastError();
 }
 
-template <int D, int BT>
+template <typename T, int D, int BT>
 hipError_t launch_mfma16(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
                          int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
                          hipStream_t stream) {
     dim3 grid(p.n_splits, p.n_kv_heads, (p.rows_per_head + kMfmaRows - 1) / kMfmaRows);
-    hipLaunchKernelGGL((attn_mfma16_kernel<D, BT>), grid, dim3(kAttnThreads), 0, stream, q,
-                       static_cast<const uint16_t *>(k_pool), static_cast<const uint16_t *>(v_pool), n_pages,
+    hipLaunchKernelGGL((attn_mfma16_kernel<T, D, BT>), grid, dim3(kAttnThreads), 0, stream, q,
+                       static_cast<const T *>(k_pool), static_cast<const T *>(v_pool), n_pages,
                        view_pages, p.n_sel, p.n_view, p.last_page_tokens, p.n_kv_heads, p.n_q_heads,
-                       p.group, p.rows_per_head, p.pages_per_split, p.n_splits, qscale, part);
+                       p.group, p.rows_per_head, p.pages_per_split, p.n_splits, qscale, p.v_scale, part);
     return hipGetLastError();
 }
 
@@ -789,18 +826,24 @@ template <typename T, int D, int BT>
 hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const void *v, int64_t n_pages,
                      const int32_t *vp, float qscale, float *part, hipStream_t stream) {
     const int rows = p.rows_per_head;
-    if constexpr (std::is_same<T, uint16_t>::value) {
-        // bf16 with 4 or more rows per KV head: matrix cores (rows padded to 16)
-        if (rows >= 4) return launch_mfma16<D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+    if constexpr (std::is_same<T, uint8_t>::value) {
+        // FP8: always the matrix cores (rows padded to 16)
+        (void)rows;
+        return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+    } else {
+        if constexpr (std::is_same<T, uint16_t>::value) {
+            // bf16 with 4 or more rows per KV head: matrix cores (rows padded to 16)
+            if (rows >= 4) return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        }
+        if constexpr (D / Vec16<T>::N == 16) {
+            if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
+            if (rows % 4 == 0) return launch_row16<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        }
+        if (rows % 8 == 0) return launch_rh<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        if (rows % 4 == 0) return launch_rh<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        if (rows % 2 == 0) return launch_rh<T, D, BT, 2>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        return launch_rh<T, D, BT, 1>(p, q, k, v, n_pages, vp, qscale, part, stream);
     }
-    if constexpr (D / Vec16<T>::N == 16) {
-        if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
-        if (rows % 4 == 0) return launch_row16<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
-    }
-    if (rows % 8 == 0) return launch_rh<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
-    if (rows % 4 == 0) return launch_rh<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
-    if (rows % 2 == 0) return launch_rh<T, D, BT, 2>(p, q, k, v, n_pages, vp, qscale, part, stream);
-    return launch_rh<T, D, BT, 1>(p, q, k, v, n_pages, vp, qscale, part, stream);
 }
 
 template <typename T, int D>
@@ -820,15 +863,20 @@ hipError_t launch_sparse_attn(const AttnPlan &p, const float *q, const void *k_p
                               const void *v_pool, int64_t n_pages, const int32_t *view_pages,
                               float scale, float *out, float *lse, char *ws, hipStream_t stream) {
     float *part = reinterpret_cast<float *>(ws + p.off_part);
-    const float qscale = scale * kLog2e;
+    const float qscale = scale * kLog2e * p.k_scale;  // k_scale is 1 unless the pools are FP8
     hipError_t e;
-    const bool bf16 = p.kv_dtype == 1;
-    if (p.head_dim == 128)
-        e = bf16 ? launch_d<uint16_t, 128>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream)
-                 : launch_d<float, 128>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
+    auto go = [&](auto elem, auto dim) {
+        return launch_d<decltype(elem), decltype(dim)::value>(p, q, k_pool, v_pool, n_pages, view_pages, qscale,
+                                                              part, stream);
+    };
+    using D64 = std::integral_constant<int, 64>;
+    using D128 = std::integral_constant<int, 128>;
+    if (p.kv_dtype == 2)
+        e = p.head_dim == 128 ? go(uint8_t{}, D128{}) : go(uint8_t{}, D64{});
+    else if (p.kv_dtype == 1)
+        e = p.head_dim == 128 ? go(uint16_t{}, D128{}) : go(uint16_t{}, D64{});
     else
-        e = bf16 ? launch_d<uint16_t, 64>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream)
-                 : launch_d<float, 64>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
+        e = p.head_dim == 128 ? go(float{}, D128{}) : go(float{}, D64{});
     if (e != hipSuccess) return e;
     const dim3 grid(p.n_kv_heads * p.rows_per_head);
     const size_t lds = sizeof(float) * (size_t)p.n_splits;

@@ -10,7 +10,10 @@
 // magnitudes span less than 2^23 is exact there, so the result -- rounded once
 // to fp32 -- does not depend on the order of summation.  The finished means
 // are staged as a [64][d] tile in LDS and written out so that each wave store
-// covers 1 KB of contiguous index.
+// covers 1 KB of contiguous index.  FP8 codes widen exactly, and their sum (Bt
+// <= 64 values on a 2^-9 grid below 448, so below 2^15) is exact even in fp32,
+// which is where it is kept; in fp64 the sum times k_scale (24 bits) is exact
+// too, so the mean is again rounded once.
 #include <math.h>
 
 #include "kvmem_device.h"
@@ -33,12 +36,16 @@ constexpr int kBlocksPerStep = 4;
 template <typename T, int D, bool ROPE>
 __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ block_to_page,
-    int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens,
+    int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens, float k_scale,
     float *__restrict__ index, const int64_t *__restrict__ block_pos, RopeFreqs fr) {
     constexpr int VEC = Vec16<T>::N;  // elements per lane per row
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
     constexpr int PAD = D + 4;        // LDS row stride (floats): conflict-free column reads
+    constexpr bool F8 = sizeof(T) == 1;
+    // exact sums: fp32 for unrotated FP8 codes, fp64 otherwise
+    using Acc = typename std::conditional<F8 && !ROPE, float, double>::type;
+    constexpr int BPS = F8 && ROPE ? 2 : kBlocksPerStep;  // 16 values per lane: fewer blocks in flight
     __shared__ float tile_buf[kIndexTile * PAD];
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -49,30 +56,31 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const int64_t b_lo = b_tile0 > first_block ? b_tile0 : first_block;
     const int64_t b_end = (int64_t)first_block + n_blocks;
     const int64_t b_hi = b_tile0 + kIndexTile < b_end ? b_tile0 + kIndexTile : b_end;
-    const double inv = 1.0 / (double)block_tokens;
+    const double inv = 1.0 / (double)block_tokens, ks = (double)k_scale;
     const int j0 = (lp % (LPR / 2)) * VEC;  // RoPE pair index of this lane's element 0
 
-    // wave w reduces tile slots w, w+4, w+8, ... (kBlocksPerStep at a time)
-    for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * kBlocksPerStep) {
-        double acc[kBlocksPerStep][VEC];
-        bool ok[kBlocksPerStep];
-        const T *base[kBlocksPerStep];
-        int64_t p0[kBlocksPerStep];
+    // wave w reduces tile slots w, w+4, w+8, ... (BPS at a time)
+    for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * BPS) {
+        Acc acc[BPS][VEC];
+        double mean[VEC];
+        bool ok[BPS];
+        const T *base[BPS];
+        int64_t p0[BPS];
 #pragma unroll
-        for (int k = 0; k < kBlocksPerStep; ++k) {
+        for (int k = 0; k < BPS; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
             const bool in = b >= b_lo && b < b_hi;
             const int64_t page = in ? block_to_page[b] : -1;
             ok[k] = in && page >= 0 && page < n_pages;
             base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D + lp * VEC;
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[k][e] = 0.0;
+            for (int e = 0; e < VEC; ++e) acc[k][e] = 0;
             p0[k] = ROPE && block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
         }
         for (int t = tg; t < block_tokens; t += TG) {
-            float v[kBlocksPerStep][VEC];
+            float v[BPS][VEC];
 #pragma unroll
-            for (int k = 0; k < kBlocksPerStep; ++k) {
+            for (int k = 0; k < BPS; ++k) {
                 if (ok[k]) {
                     Vec16<T>::load(base[k] + (int64_t)t * D, v[k]);
                 } else {
@@ -83,7 +91,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
             if constexpr (ROPE) {
                 const bool upper = lp >= LPR / 2;
 #pragma unroll
-                for (int k = 0; k < kBlocksPerStep; ++k) {
+                for (int k = 0; k < BPS; ++k) {
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) {
                         const float other = __shfl_xor(v[k][e], LPR / 2, kWave);
@@ -98,23 +106,24 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                 }
             }
 #pragma unroll
-            for (int k = 0; k < kBlocksPerStep; ++k)
+            for (int k = 0; k < BPS; ++k)
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) acc[k][e] += (double)v[k][e];
+                for (int e = 0; e < VEC; ++e) acc[k][e] += (Acc)v[k][e];
         }
 #pragma unroll
-        for (int k = 0; k < kBlocksPerStep; ++k) {
+        for (int k = 0; k < BPS; ++k) {
 #pragma unroll
             for (int o = LPR; o < kWave; o <<= 1)
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) acc[k][e] += shfl_xor_d(acc[k][e], o);
+                for (int e = 0; e < VEC; ++e) acc[k][e] += __shfl_xor(acc[k][e], o, kWave);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) mean[e] = (double)acc[k][e] * ks * inv;
             if (tg == 0) {
                 float *dst = tile_buf + (s0 + k * kWaves) * PAD + lp * VEC;
 #pragma unroll
                 for (int e = 0; e < VEC; e += 4)
                     *reinterpret_cast<float4 *>(dst + e) = ok[k]
-                        ? make_float4((float)(acc[k][e] * inv), (float)(acc[k][e + 1] * inv),
-                                      (float)(acc[k][e + 2] * inv), (float)(acc[k][e + 3] * inv))
+                        ? make_float4((float)mean[e], (float)mean[e + 1], (float)mean[e + 2], (float)mean[e + 3])
                         : make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
                                       __builtin_nanf(""));
             }
@@ -133,7 +142,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 }
 
 template <typename T, int D>
-hipError_t launch_t(int n_kv_heads, int block_tokens, const void *k_pool, int64_t n_pages,
+hipError_t launch_t(int n_kv_heads, int block_tokens, float k_scale, const void *k_pool, int64_t n_pages,
                     const int32_t *block_to_page, int32_t first_block, int32_t n_blocks,
                     float *index, hipStream_t stream, bool rope, const int64_t *block_pos,
                     const RopeFreqs *fr) {
@@ -145,32 +154,33 @@ hipError_t launch_t(int n_kv_heads, int block_tokens, const void *k_pool, int64_
         f = *fr;
         hipLaunchKernelGGL((build_index_kernel<T, D, true>), grid, dim3(kWaves * kWave), 0, stream,
                            static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
-                           n_kv_heads, block_tokens, index, block_pos, f);
+                           n_kv_heads, block_tokens, k_scale, index, block_pos, f);
     } else {
         hipLaunchKernelGGL((build_index_kernel<T, D, false>), grid, dim3(kWaves * kWave), 0, stream,
                            static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
-                           n_kv_heads, block_tokens, index, block_pos, f);
+                           n_kv_heads, block_tokens, k_scale, index, block_pos, f);
     }
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
+hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens, float k_scale,
                               const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                               int32_t first_block, int32_t n_blocks, float *index,
                               hipStream_t stream, bool rope, const int64_t *block_pos, const RopeFreqs *fr) {
     if (n_blocks == 0) return hipSuccess;
-    const bool bf16 = kv_dtype == 1;
-    if (head_dim == 128)
-        return bf16 ? launch_t<uint16_t, 128>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                              first_block, n_blocks, index, stream, rope, block_pos, fr)
-                    : launch_t<float, 128>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                           first_block, n_blocks, index, stream, rope, block_pos, fr);
-    return bf16 ? launch_t<uint16_t, 64>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                         first_block, n_blocks, index, stream, rope, block_pos, fr)
-                : launch_t<float, 64>(n_kv_heads, block_tokens, k_pool, n_pages, block_to_page,
-                                      first_block, n_blocks, index, stream, rope, block_pos, fr);
+    auto go = [&](auto elem, auto dim) {
+        using T = decltype(elem);
+        return launch_t<T, decltype(dim)::value>(n_kv_heads, block_tokens, k_scale, k_pool, n_pages,
+                                                 block_to_page, first_block, n_blocks, index, stream, rope,
+                                                 block_pos, fr);
+    };
+    using D64 = std::integral_constant<int, 64>;
+    using D128 = std::integral_constant<int, 128>;
+    if (kv_dtype == 2) return head_dim == 128 ? go(uint8_t{}, D128{}) : go(uint8_t{}, D64{});
+    if (kv_dtype == 1) return head_dim == 128 ? go(uint16_t{}, D128{}) : go(uint16_t{}, D64{});
+    return head_dim == 128 ? go(float{}, D128{}) : go(float{}, D64{});
 }
 
 }  // namespace kvmem

@@ -46,8 +46,23 @@ kvmem_status check_geom(const kvmem_geom *g) {
     if (g->block_tokens != 16 && g->block_tokens != 32 && g->block_tokens != 64)
         return fail(KVMEM_ERR_UNSUPPORTED, "block_tokens %d: 16, 32 or 64 is required",
                     g->block_tokens);
-    if (g->kv_dtype != KVMEM_F32 && g->kv_dtype != KVMEM_BF16)
-        return fail(KVMEM_ERR_DTYPE, "kv_dtype %d is not KVMEM_F32 or KVMEM_BF16", g->kv_dtype);
+    if (g->kv_dtype != KVMEM_F32 && g->kv_dtype != KVMEM_BF16 && g->kv_dtype != KVMEM_FP8_E4M3)
+        return fail(KVMEM_ERR_DTYPE, "kv_dtype %d is not KVMEM_F32, KVMEM_BF16 or KVMEM_FP8_E4M3",
+                    g->kv_dtype);
+    if (g->kv_dtype == KVMEM_FP8_E4M3 &&
+        !(std::isfinite(g->k_scale) && g->k_scale > 0.f && std::isfinite(g->v_scale) && g->v_scale > 0.f))
+        return fail(KVMEM_ERR_SHAPE, "FP8 pools need finite positive k_scale and v_scale (got %g, %g)",
+                    (double)g->k_scale, (double)g->v_scale);
+    return KVMEM_OK;
+}
+
+// FP8 codes carry one scale per pool; the other types are used as stored.
+float k_scale_of(const kvmem_geom *g) { return g->kv_dtype == KVMEM_FP8_E4M3 ? g->k_scale : 1.f; }
+float v_scale_of(const kvmem_geom *g) { return g->kv_dtype == KVMEM_FP8_E4M3 ? g->v_scale : 1.f; }
+
+kvmem_status no_fp8(const kvmem_geom *g, const char *what) {
+    if (g->kv_dtype == KVMEM_FP8_E4M3)
+        return fail(KVMEM_ERR_UNSUPPORTED, "%s takes f32 or bf16 pools, not FP8", what);
     return KVMEM_OK;
 }
 
@@ -135,6 +150,8 @@ kvmem_status make_attn_plan(const kvmem_geom *g, int32_t n_q, int32_t n_sel, int
     p.head_dim = g->head_dim;
     p.block_tokens = g->block_tokens;
     p.kv_dtype = g->kv_dtype;
+    p.k_scale = k_scale_of(g);
+    p.v_scale = v_scale_of(g);
     p.n_sel = n_sel;
     p.n_view = n_view;
     p.last_page_tokens = last_page_tokens;
@@ -180,8 +197,8 @@ kvmem_status kvmem_build_index(const kvmem_geom *geom, const void *k_pool, int64
     if (!aligned16(k_pool) || !aligned16(index) || !aligned16(block_to_page))
         return fail(KVMEM_ERR_ALIGN, "k_pool, block_to_page and index must be 16-byte aligned");
     return hip_status(kvmem::launch_build_index(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
-                                                geom->block_tokens, k_pool, n_pages, block_to_page,
-                                                first_block, n_blocks, index,
+                                                geom->block_tokens, k_scale_of(geom), k_pool, n_pages,
+                                                block_to_page, first_block, n_blocks, index,
                                                 static_cast<hipStream_t>(stream)),
                       "build_index launch");
 }
@@ -206,8 +223,8 @@ kvmem_status kvmem_build_index_rope(const kvmem_geom *geom, const void *k_pool, 
     kvmem::RopeFreqs fr;
     kvmem::rope_freqs(rope_base, geom->head_dim, fr);
     return hip_status(kvmem::launch_build_index(geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
-                                                geom->block_tokens, k_pool, n_pages, block_to_page,
-                                                first_block, n_blocks, index,
+                                                geom->block_tokens, k_scale_of(geom), k_pool, n_pages,
+                                                block_to_page, first_block, n_blocks, index,
                                                 static_cast<hipStream_t>(stream), true, block_pos, &fr),
                       "build_index_rope launch");
 }
@@ -218,6 +235,7 @@ kvmem_status kvmem_materialize(const kvmem_geom *geom, double rope_base, const v
                                void *k_dst_pool, void *v_dst_pool, int64_t n_dst_pages, void *stream) {
     kvmem_status st = check_geom(geom);
     if (st != KVMEM_OK) return st;
+    if ((st = no_fp8(geom, "kvmem_materialize")) != KVMEM_OK) return st;
     if (!(rope_base > 1.0) || !std::isfinite(rope_base))
         return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
     if (n_blocks < 0 || n_blocks > (1 << 24))
@@ -243,6 +261,7 @@ kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool
                           const int32_t *pages, const int64_t *delta_positions, int32_t n_list, void *stream) {
     kvmem_status st = check_geom(geom);
     if (st != KVMEM_OK) return st;
+    if ((st = no_fp8(geom, "kvmem_rerope")) != KVMEM_OK) return st;
     if (!(rope_base > 1.0) || !std::isfinite(rope_base))
         return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
     if (n_list < 0 || n_list > (1 << 24)) return fail(KVMEM_ERR_SHAPE, "n_list %d must be in [0, 2^24]", n_list);

@@ -52,6 +52,26 @@ struct Vec16<uint16_t> {
     }
 };
 
+// FP8 pools hold OCP E4M3 codes (one byte each).  gfx950's conversion
+// instructions read this format: every code, subnormals, -0 and NaN included,
+// widens exactly to fp32 and to bf16.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+template <>
+struct Vec16<uint8_t> {
+    static constexpr int N = 16;
+    __device__ static inline void load(const uint8_t *p, float (&out)[16]) {
+        const uint4 v = load_stream16(p);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const f32x2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8(w[i], false);  // bytes 0, 1
+            const f32x2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8(w[i], true);   // bytes 2, 3
+            out[4 * i] = lo[0]; out[4 * i + 1] = lo[1];
+            out[4 * i + 2] = hi[0]; out[4 * i + 3] = hi[1];
+        }
+    }
+};
+
 // cos and sin of the RoPE angle pos * f (fp64).  The angle is reduced to about
 // [-pi, pi] with a two-part 2*pi (Cody-Waite, fused multiply-adds), so the
 // reduced angle is accurate to about 1e-16 rad for any fp64 angle, then cos

@@ -91,6 +91,7 @@ constexpr int kPartStride = 4;           // floats after the D outputs of a part
 
 struct AttnPlan {
     int n_kv_heads, n_q_heads, group, n_q, rows_per_head, head_dim, block_tokens, kv_dtype;
+    float k_scale, v_scale;  // FP8 pool scales (1 for the other types)
     int n_sel, n_view, last_page_tokens;
     int pages_per_split, n_splits;
     size_t off_part;  // float [Hkv][n_splits][rows_per_head][head_dim + kPartStride]
@@ -118,10 +119,11 @@ inline void rope_freqs(double base, int head_dim, RopeFreqs &fr) {
 }
 
 // ---- launchers (return the launch status) -------------------------------
+// kv_dtype: 0 fp32, 1 bf16 bits, 2 FP8 E4M3 codes (scaled by k_scale, v_scale).
 // block_pos / fr are used only when rope is set: the keys carry RoPE at
 // positions block_pos[b] + t (block_pos NULL: b * block_tokens + t).
 hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
-                              const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
+                              float k_scale, const void *k_pool, int64_t n_pages, const int32_t *block_to_page,
                               int32_t first_block, int32_t n_blocks, float *index,
                               hipStream_t stream, bool rope = false, const int64_t *block_pos = nullptr,
                               const RopeFreqs *fr = nullptr);

@@ -15,7 +15,7 @@ import re
 import torch
 
 KVMEM_OK = 0
-KVMEM_F32, KVMEM_BF16 = 0, 1
+KVMEM_F32, KVMEM_BF16, KVMEM_FP8_E4M3 = 0, 1, 2
 KVMEM_REDUCE_MEAN_ALL, KVMEM_REDUCE_MAX_GROUP = 0, 1
 
 STATUS_NAMES = {
@@ -38,7 +38,7 @@ class KvmemError(RuntimeError):
 class kvmem_geom(ctypes.Structure):
     _fields_ = [("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_tokens", ctypes.c_int32),
-                ("kv_dtype", ctypes.c_int32)]
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -47,11 +47,13 @@ class Geom:
     n_q_heads: int
     head_dim: int
     block_tokens: int
-    kv_dtype: int  # KVMEM_F32 or KVMEM_BF16
+    kv_dtype: int  # KVMEM_F32, KVMEM_BF16 or KVMEM_FP8_E4M3
+    k_scale: float = 1.0  # FP8 pools: K = decoded code * k_scale
+    v_scale: float = 1.0  # FP8 pools: V = decoded code * v_scale
 
     def c(self) -> kvmem_geom:
         return kvmem_geom(self.n_kv_heads, self.n_q_heads, self.head_dim, self.block_tokens,
-                          self.kv_dtype)
+                          self.kv_dtype, self.k_scale, self.v_scale)
 
 
 _lib = None
@@ -122,7 +124,9 @@ def kv_dtype_of(t: torch.Tensor) -> int:
         return KVMEM_BF16
     if t.dtype == torch.float32:
         return KVMEM_F32
-    raise TypeError(f"K/V pools must be bfloat16 or float32, got {t.dtype}")
+    if t.dtype in (torch.float8_e4m3fn, torch.uint8):  # FP8 E4M3 codes
+        return KVMEM_FP8_E4M3
+    raise TypeError(f"K/V pools must be bfloat16, float32 or float8_e4m3fn (or uint8 codes), got {t.dtype}")
 
 
 def _need(t: torch.Tensor, dtype, name: str):

@@ -15,8 +15,9 @@ from .workload import MEAN_ALL, Config
 
 
 def geom_of(cfg: Config) -> K.Geom:
-    return K.Geom(cfg.n_kv_heads, cfg.n_q_heads, cfg.head_dim, cfg.block_tokens,
-                  K.KVMEM_BF16 if cfg.kv_dtype == "bf16" else K.KVMEM_F32)
+    dt = {"f32": K.KVMEM_F32, "bf16": K.KVMEM_BF16, "fp8": K.KVMEM_FP8_E4M3}[cfg.kv_dtype]
+    return K.Geom(cfg.n_kv_heads, cfg.n_q_heads, cfg.head_dim, cfg.block_tokens, dt,
+                  cfg.kv_scale, cfg.kv_scale)
 
 
 def mode_of(cfg: Config) -> int:
@@ -24,7 +25,10 @@ def mode_of(cfg: Config) -> int:
 
 
 def pool_to_device(pool: np.ndarray, device) -> torch.Tensor:
-    """Upload a host pool (float32, or bf16 bits as uint16) as float32 / bfloat16."""
+    """Upload a host pool (float32, bf16 bits as uint16, or E4M3 codes as uint8)
+    as float32 / bfloat16 / float8_e4m3fn."""
+    if pool.dtype == np.uint8:
+        return torch.from_numpy(pool).to(device).view(torch.float8_e4m3fn)
     if pool.dtype == np.uint16:
         return torch.from_numpy(pool.view(np.int16)).to(device).view(torch.bfloat16)
     return torch.from_numpy(pool).to(device)

@@ -28,7 +28,11 @@ in for them:
   gathers are scattered; pools hold exactly M pages.
 
 bf16 values are produced from fp32 draws by round-to-nearest-even and kept as
-raw uint16 bit patterns.  All draws come from numpy's PCG64 with one
+raw uint16 bit patterns.  FP8 pools (the KV-cache precision of the paper's
+evaluation platforms, Sec. 6) hold OCP E4M3 codes of x / kv_scale, rounded to
+nearest even and saturated at +-448, with one static scale per pool:
+kv_scale = 8/448 for the offset configs (|x| up to 8, about 7 standard
+deviations) and 16/448 for the mixture.  All draws come from numpy's PCG64 with one
 SeedSequence child per independent chunk, so results do not depend on the
 number of worker threads.
 """
@@ -52,7 +56,7 @@ class Config:
     n_kv_heads: int
     n_q_heads: int
     head_dim: int
-    kv_dtype: str  # "f32" or "bf16"
+    kv_dtype: str  # "f32", "bf16" or "fp8" (E4M3 codes times kv_scale)
     history_tokens: int
     block_tokens: int
     recent_tokens: int
@@ -64,6 +68,7 @@ class Config:
     kind: str  # "offset" or "mixture"
     seed: int
     top_k: int  # the stated number of selectable historical blocks
+    kv_scale: float = 1.0  # fp8: the static scale of every K and V pool
 
     @property
     def n_blocks(self) -> int:
@@ -92,7 +97,7 @@ class Config:
 
     @property
     def elem_bytes(self) -> int:
-        return 4 if self.kv_dtype == "f32" else 2
+        return {"f32": 4, "bf16": 2, "fp8": 1}[self.kv_dtype]
 
     def replace(self, **kw) -> "Config":
         return dataclasses.replace(self, **kw)
@@ -117,6 +122,21 @@ CONFIGS = {
                       4, 8, 32, 128, "bf16", 1048576, 64, 8192, 0, 262144, 4, MAX_GROUP, 0,
                       "mixture", 4, 3968),
 }
+# The FP8 variants of the 1M-token workloads (same draws, stored as E4M3 codes).
+CONFIGS["1m_fp8"] = CONFIGS["1m"].replace(
+    name="1m_fp8", kv_dtype="fp8", kv_scale=float(np.float32(8 / 448)),
+    description=CONFIGS["1m"].description.replace("bf16 K/V", "FP8 E4M3 K/V (scale 8/448)"))
+CONFIGS["1m_mtp4_fp8"] = CONFIGS["1m_mtp4"].replace(
+    name="1m_mtp4_fp8", kv_dtype="fp8", kv_scale=float(np.float32(16 / 448)),
+    description=CONFIGS["1m_mtp4"].description.replace("bf16 K/V", "FP8 E4M3 K/V (scale 16/448)"))
+
+
+def fp8_codes(x: np.ndarray, scale: float) -> np.ndarray:
+    """fp32 -> OCP E4M3 codes (uint8) of x / scale: fp32 division, then round to
+    nearest even, saturating at +-448 (torch's CPU cast after clamping)."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32) / np.float32(scale))
+    return t.clamp_(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -137,7 +157,7 @@ class Workload:
     cfg: Config
     seed: int
     q: np.ndarray  # float32 [n_sets][L][n_q][Hq][d]
-    k_pool: list  # per layer: [P][Hkv][Bt][d] uint16 (bf16 bits) or float32
+    k_pool: list  # per layer: [P][Hkv][Bt][d] uint16 (bf16 bits), uint8 (E4M3 codes) or float32
     v_pool: list
     block_to_page: np.ndarray  # int32 [M]
     planted: np.ndarray  # int32 block ids (may be empty)
@@ -147,15 +167,20 @@ def _workers() -> int:
     return max(1, min(16, os.cpu_count() or 1))
 
 
-def _store(x: np.ndarray, kv_dtype: str) -> np.ndarray:
-    return bf16_bits(x) if kv_dtype == "bf16" else np.ascontiguousarray(x, dtype=np.float32)
+def _store(x: np.ndarray, cfg: Config) -> np.ndarray:
+    if cfg.kv_dtype == "fp8":
+        return fp8_codes(x, cfg.kv_scale)
+    return bf16_bits(x) if cfg.kv_dtype == "bf16" else np.ascontiguousarray(x, dtype=np.float32)
+
+
+def _pool_dtype(cfg: Config):
+    return {"f32": np.float32, "bf16": np.uint16, "fp8": np.uint8}[cfg.kv_dtype]
 
 
 def _offset_pool(ss: np.random.SeedSequence, cfg: Config, chunk: int) -> np.ndarray:
     """[P][Hkv][Bt][d]: per-(page, head) offset N(0, 0.5^2) plus N(0,1) tokens."""
     m, hkv, bt, d = cfg.n_blocks, cfg.n_kv_heads, cfg.block_tokens, cfg.head_dim
-    dtype = np.uint16 if cfg.kv_dtype == "bf16" else np.float32
-    pool = np.empty((m, hkv, bt, d), dtype)
+    pool = np.empty((m, hkv, bt, d), _pool_dtype(cfg))
     starts = list(range(0, m, chunk))
     children = ss.spawn(len(starts))
 
@@ -166,7 +191,7 @@ def _offset_pool(ss: np.random.SeedSequence, cfg: Config, chunk: int) -> np.ndar
         off = rng.standard_normal((hi - lo, hkv, 1, d), dtype=np.float32) * np.float32(0.5)
         z = rng.standard_normal((hi - lo, hkv, bt, d), dtype=np.float32)
         z += off
-        pool[lo:hi] = _store(z, cfg.kv_dtype)
+        pool[lo:hi] = _store(z, cfg)
 
     with _cf.ThreadPoolExecutor(_workers()) as ex:
         list(ex.map(fill, range(len(starts))))
@@ -183,7 +208,7 @@ def _mixture_pool(ss: np.random.SeedSequence, cfg: Config, chunk: int,
     rj = np.random.Generator(np.random.PCG64(ss_j))
     w = (np.arange(1, n_clusters + 1, dtype=np.float64)) ** (-zipf_s)
     cluster = rj.choice(n_clusters, size=(m, hkv), p=w / w.sum())
-    pool = np.empty((m, hkv, bt, d), np.uint16 if cfg.kv_dtype == "bf16" else np.float32)
+    pool = np.empty((m, hkv, bt, d), _pool_dtype(cfg))
     starts = list(range(0, m, chunk))
     children = ss_z.spawn(len(starts))
     heads = np.arange(hkv)[None, :]
@@ -194,7 +219,7 @@ def _mixture_pool(ss: np.random.SeedSequence, cfg: Config, chunk: int,
         rng = np.random.Generator(np.random.PCG64(children[i]))
         z = rng.standard_normal((hi - lo, hkv, bt, d), dtype=np.float32)
         z += centres[heads, cluster[lo:hi]][:, :, None, :]
-        pool[lo:hi] = _store(z, cfg.kv_dtype)
+        pool[lo:hi] = _store(z, cfg)
 
     with _cf.ThreadPoolExecutor(_workers()) as ex:
         list(ex.map(fill, range(len(starts))))
@@ -226,7 +251,7 @@ def _plant(ss: np.random.SeedSequence, cfg: Config, pool: np.ndarray, q0: np.nda
         nu -= (nu @ u)[..., None] * u
         nu /= np.linalg.norm(nu, axis=-1, keepdims=True)
         keys = np.sqrt(d) * (0.9 * u + np.sqrt(0.19) * nu)
-        pool[block_to_page[planted], g] = _store(keys.astype(np.float32), cfg.kv_dtype)
+        pool[block_to_page[planted], g] = _store(keys.astype(np.float32), cfg)
     return planted.astype(np.int32)
 
 

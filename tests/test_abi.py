@@ -200,3 +200,25 @@ def test_rope_calls_validation(L):
     assert r(n=0, k=None, pages=None) == "KVMEM_OK"
     bad = g1(head_dim=96)
     assert _status(L.kvmem_rerope(ctypes.byref(bad), 1e6, FAKE, 10, FAKE, FAKE, 4, None)) == "KVMEM_ERR_UNSUPPORTED"
+
+
+def test_fp8_geometry_validation(L):
+    z = ctypes.c_int32()
+    for ks, vs, st in [(0.02, 0.02, "KVMEM_OK"), (0.0, 0.02, "KVMEM_ERR_SHAPE"), (0.02, -1.0, "KVMEM_ERR_SHAPE"),
+                       (float("inf"), 0.02, "KVMEM_ERR_SHAPE"), (0.02, float("nan"), "KVMEM_ERR_SHAPE")]:
+        g = g1(kv_dtype=K.KVMEM_FP8_E4M3, k_scale=ks, v_scale=vs)
+        assert _status(L.kvmem_plan_view(ctypes.byref(g), 100, 0, 4, 10**6, 10**6, ctypes.byref(z), None)) == st
+    # the scales are not read for the other types
+    assert _status(L.kvmem_plan_view(ctypes.byref(g1(k_scale=0.0, v_scale=float("nan"))), 100, 0, 4, 10**6,
+                                     10**6, ctypes.byref(z), None)) == "KVMEM_OK"
+
+
+@no_gpu
+def test_fp8_position_calls_unsupported(L):
+    g = ctypes.byref(g1(kv_dtype=K.KVMEM_FP8_E4M3, k_scale=0.02, v_scale=0.02))
+    assert _status(L.kvmem_materialize(g, 1e6, FAKE, FAKE, 10, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 10, None)) \
+        == "KVMEM_ERR_UNSUPPORTED"
+    assert _status(L.kvmem_rerope(g, 1e6, FAKE, 10, FAKE, FAKE, 4, None)) == "KVMEM_ERR_UNSUPPORTED"
+    assert "FP8" in K.kvmem_last_error()
+    # the index from encoded keys does take FP8 pools (host checks pass down to the NULL check)
+    assert _status(L.kvmem_build_index_rope(g, None, 10, FAKE, None, 1e6, 0, 4, FAKE, None)) == "KVMEM_ERR_NULL"

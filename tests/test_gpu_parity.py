@@ -14,7 +14,7 @@ from paper_2609_04852_amd import kvmem as K
 from paper_2609_04852_amd import workload as W
 from paper_2609_04852_amd.step import LayerState
 
-from parity import (assert_index_bitwise, check_attention, check_scores, check_selection, log)
+from parity import (assert_index_bitwise, check_attention, check_scores, check_selection, log, oracle_pool)
 
 pytestmark = pytest.mark.gpu
 
@@ -43,12 +43,13 @@ def run_case(cfg, seed, layer=0, budget=None, lpt=None, e2e=True, stats=None):
     q_l = w.q[0, layer:layer + 1]  # [1][n_q][Hq][d]
     S, Rr = cfg.sink_blocks, cfg.n_recent
     # ---- oracle
-    index_ref = oracle.mean_k(kp, b2p)
+    kp_o, vp_o = oracle_pool(cfg, kp), oracle_pool(cfg, vp_pool)
+    index_ref = oracle.mean_k(kp_o, b2p)
     rel = oracle.block_relevance(q_l, index_ref[None], S, Rr, oracle_mode(cfg))
     k_eff = oracle.k_eff(budget, budget, cfg.block_tokens, cfg.n_blocks, S, Rr)
     vb_ref, vp_ref = oracle.select(rel, S, Rr, k_eff, b2p)
     last = cfg.block_tokens if lpt is None else lpt
-    out_ref, lse_ref = oracle.view_attention(q_l[0], kp, vp_pool, vp_ref, last_page_tokens=last)
+    out_ref, lse_ref = oracle.view_attention(q_l[0], kp_o, vp_o, vp_ref, last_page_tokens=last)
     # ---- GPU
     log("  gpu: build_index")
     st = LayerState(cfg, kp, vp_pool, b2p, budget_tokens=budget)
@@ -297,3 +298,112 @@ def test_all_equal_scores_large():
     expect = list(range(3)) + list(range(3, 3 + 7000)) + list(range(20480 - 5, 20480))
     assert vb.tolist() == expect
     np.testing.assert_array_equal(st.view_pages.cpu().numpy()[0], w.block_to_page[vb])
+
+
+# ---- FP8 K/V (OCP E4M3 codes, one scale per pool) ------------------------
+FP8_SHAPES = [
+    # Hkv, Hq, d, Bt, M, S, Rr, n_q, mode, extra, scale
+    (8, 32, 128, 16, 2000, 0, 33, 1, W.MEAN_ALL, 517, 8 / 448),     # 4 rows per KV head
+    (2, 2, 128, 32, 700, 3, 5, 1, W.MEAN_ALL, 100, 0.0173),          # 1 row: padded MFMA tile
+    (4, 8, 64, 64, 333, 0, 1, 1, W.MAX_GROUP, 41, 2.0 ** -5),        # 2 rows, d64, Bt64
+    (2, 16, 128, 16, 700, 0, 5, 2, W.MEAN_ALL, 100, 0.011),          # 16 rows
+    (4, 16, 64, 32, 500, 1, 3, 4, W.MAX_GROUP, 60, 8 / 448),          # 16 rows, d64
+    (1, 8, 64, 16, 1500, 2, 7, 2, W.MAX_GROUP, 230, 0.5),             # saturating scale
+]
+
+
+def fp8_cfg(hkv, hq, d, bt, m, s, rr, nq, mode, extra, scale, planted=3):
+    return shape_cfg(hkv, hq, d, bt, "fp8", m, s, rr, nq, mode, extra, planted).replace(
+        kv_scale=float(np.float32(scale)))
+
+
+@pytest.mark.parametrize("shape", FP8_SHAPES, ids=[f"f{i}" for i in range(len(FP8_SHAPES))])
+def test_fp8_shapes(shape):
+    run_case(fp8_cfg(*shape), 17)
+
+
+def test_fp8_partial_last_page():
+    cfg = fp8_cfg(2, 8, 128, 32, 400, 0, 3, 2, W.MEAN_ALL, 60, 8 / 448)
+    run_case(cfg, 5, lpt=7)
+    run_case(cfg, 6, lpt=1)
+
+
+def test_1m_fp8():
+    run_case(W.CONFIGS["1m_fp8"], W.CONFIGS["1m_fp8"].seed)
+
+
+def test_1m_mtp4_fp8_layer0():
+    run_case(W.CONFIGS["1m_mtp4_fp8"], W.CONFIGS["1m_mtp4_fp8"].seed, layer=0)
+
+
+@pytest.mark.parametrize("bt,lpt", [(16, 16), (32, 5), (64, 33)])
+def test_fp8_random_views_32_rows(bt, lpt):
+    cfg = fp8_cfg(2, 16, 128, bt, 300, 0, 2, 4, W.MAX_GROUP, 10, 0.0173)
+    log(f"[case] fp8, 32 rows per KV head, Bt={bt}, last page {lpt}")
+    w = W.generate(cfg, 21)
+    rng = np.random.default_rng(5)
+    vp = np.stack([rng.choice(cfg.n_blocks, 97, replace=False) for _ in range(2)]).astype(np.int32)
+    q = np.ascontiguousarray(w.q[0, 0])
+    o_ref, l_ref = oracle.view_attention(q, oracle_pool(cfg, w.k_pool[0]), oracle_pool(cfg, w.v_pool[0]), vp,
+                                         last_page_tokens=lpt)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    out, lse = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(vp).cuda(), last_page_tokens=lpt)
+    torch.cuda.synchronize()
+    err = check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, "fp8")
+    log(f"  max abs err out {err[0]:.2e} lse {err[1]:.2e}")
+
+
+def test_fp8_every_code():
+    """Pools drawn uniformly over all 254 finite codes (subnormals, -0, +-448
+    included): the index is bitwise and attention within tolerance; a NaN code
+    makes its block's index row NaN."""
+    cfg = fp8_cfg(2, 8, 128, 16, 300, 0, 2, 1, W.MEAN_ALL, 40, 0.0173, planted=0)
+    log("[case] fp8 pools over every finite code")
+    w = W.generate(cfg, 23)
+    rng = np.random.default_rng(9)
+    finite = np.setdiff1d(np.arange(256), [0x7F, 0xFF]).astype(np.uint8)
+    kp = rng.choice(finite, w.k_pool[0].shape)
+    vp_pool = rng.choice(finite, w.v_pool[0].shape)
+    kp_o, vp_o = oracle_pool(cfg, kp), oracle_pool(cfg, vp_pool)
+    st = LayerState(cfg, kp, vp_pool, w.block_to_page)
+    st.build_index()
+    torch.cuda.synchronize()
+    assert_index_bitwise(st.index_rows(), oracle.mean_k(kp_o, w.block_to_page))
+    # small queries keep the softmax spread over many tokens of these wide-range keys
+    q = np.ascontiguousarray(w.q[0, 0] * np.float32(0.01))
+    views = np.arange(40, dtype=np.int32)[None]
+    o_ref, l_ref = oracle.view_attention(q, kp_o, vp_o, views, last_page_tokens=9)
+    out, lse = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(views).cuda(), last_page_tokens=9)
+    torch.cuda.synchronize()
+    # values reach 448 * 0.0173 = 7.75: the bound scales with the largest |V|
+    err = float(np.abs(out.cpu().numpy().astype(np.float64) - o_ref).max())
+    lerr = float(np.abs(lse.cpu().numpy().astype(np.float64) - l_ref).max())
+    log(f"  max abs err out {err:.2e} lse {lerr:.2e}")
+    assert err <= 2e-2 and lerr <= 2e-2
+    kp2 = kp.copy()
+    kp2[w.block_to_page[5], 1, 3, 17] = 0x7F
+    st2 = LayerState(cfg, kp2, None, w.block_to_page)
+    st2.build_index()
+    torch.cuda.synchronize()
+    idx = st2.index_rows()
+    assert np.isnan(idx[5, 1, 17]) and np.isfinite(np.delete(idx[5, 1], 17)).all()
+    ok = np.ones(cfg.n_blocks, bool)
+    ok[5] = False
+    assert_index_bitwise(idx[ok], oracle.mean_k(kp_o, w.block_to_page)[ok])
+
+
+def test_fp8_out_of_range_pages_give_nan():
+    cfg = fp8_cfg(2, 16, 128, 16, 200, 0, 2, 2, W.MAX_GROUP, 20, 0.0173)
+    log("[case] fp8 out-of-range page ids")
+    w = W.generate(cfg, 13)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    q = np.ascontiguousarray(w.q[0, 0])
+    vp = np.stack([np.arange(30), np.arange(30, 60)]).astype(np.int32)
+    vp[1, 17] = cfg.n_blocks + 1000
+    out, _ = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(vp).cuda())
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert np.isnan(o[:, 8:]).all() and np.isfinite(o[:, :8]).all()
+    o_ref, _ = oracle.view_attention(q[:, :8], oracle_pool(cfg, w.k_pool[0])[:, :1],
+                                     oracle_pool(cfg, w.v_pool[0])[:, :1], vp[:1])
+    np.testing.assert_allclose(o[:, :8], o_ref, atol=2e-2, rtol=0)

@@ -79,6 +79,31 @@ def test_index_from_encoded_keys(name, baked):
     assert np.abs(plain - ref).max() > 1e-2
 
 
+@pytest.mark.parametrize("d,bt", [(128, 16), (64, 32)])
+def test_index_from_encoded_fp8_keys(d, bt):
+    """FP8 pools whose codes hold RoPE-encoded keys (encoded by the oracle in
+    fp64, then quantised like every FP8 pool)."""
+    cfg = W.CONFIGS["64k"].replace(kv_dtype="fp8", kv_scale=float(np.float32(8 / 448)), head_dim=d,
+                                   block_tokens=bt, history_tokens=2048 * bt, n_kv_heads=4, n_q_heads=16)
+    log(f"[case] index from encoded FP8 keys d={d} Bt={bt}")
+    w = W.generate(cfg, 5, with_values=False)
+    m = cfg.n_blocks
+    p0 = np.random.default_rng(8).integers(0, 2 ** 30, m).astype(np.int64)
+    raw = oracle.decode_fp8(w.k_pool[0], cfg.kv_scale)
+    pos = np.zeros(raw.shape[:3], np.int64)
+    pos[w.block_to_page] = p0[:, None, None] + np.arange(bt)[None, None, :]
+    codes = W.fp8_codes(oracle.rope(raw, pos, BASE).astype(np.float32), cfg.kv_scale)
+    ref = oracle.mean_k_rope(oracle.decode_fp8(codes, cfg.kv_scale), w.block_to_page, BASE, block_pos=p0)
+    st = LayerState(cfg, codes, None, w.block_to_page)
+    K.kvmem_build_index_rope(st.geom, st.k_pool, st.block_to_page, 0, m, st.index, BASE,
+                             torch.from_numpy(p0).cuda())
+    torch.cuda.synchronize()
+    got = st.index_rows()
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    log(f"  max abs err {err.max():.2e}, exact {np.mean(err == 0):.3f}")
+    np.testing.assert_allclose(got, ref, atol=2e-6, rtol=2e-6)
+
+
 @pytest.mark.parametrize("dt,d,bt", [("bf16", 128, 16), ("bf16", 64, 64), ("f32", 128, 32)])
 def test_materialize(dt, d, bt):
     cfg = W.small_config(n_kv_heads=4, n_q_heads=16, head_dim=d, block_tokens=bt, kv_dtype=dt,
