@@ -439,10 +439,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
 //   softmax online per row in base 2; each lane holds 8 scores of its row per
 //           32-token tile, the row max is completed over the 4 kg lanes.
 //   output  O^T = V^T P^T per 32 tokens and 16 dims: P^T (B operand) is the
-//           lane's own 8 probabilities, split hi + lo; V^T (A operand) is read
-//           from a per-wave LDS copy of the tile (row pitch D + 4 halves keeps
-//           the column reads free of bank conflicts).  The contraction order of
-//           tokens is the same permutation on both sides.
+//           lane's own 8 probabilities, split hi + lo; V^T (A operand) comes
+//           from a per-wave LDS copy of the tile through two transposing reads
+//           (ds_read_b64_tr_b16) per 16 dims.  The contraction order of tokens
+//           is the same permutation on both sides.
 // Waves take the split's 32-token tiles in turn and are merged in LDS; one
 // partial (O, max, sum) per row is written in the format attn_combine reads.
 // FP8 K/V (E4M3 codes): every code is exactly a bf16 value, so the same MFMA
@@ -456,21 +456,24 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kMfmaRows = 16;
 constexpr int kMfmaTile = 32;  // tokens per tile
 
-__device__ inline uint16_t bf16_rne(float x) {  // round to nearest even (finite x)
-    const uint32_t u = __float_as_uint(x);
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-__device__ inline float bf16_val(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-// hi + lo bf16 split of 8 floats
+// hi + lo bf16 split of 8 floats: hi = bf16(x), lo = bf16(x - hi), both rounded
+// to nearest even by the conversion instruction (v_cvt_pk_bf16_f32)
 __device__ inline void split_bf16x8(const float (&x)[8], bf16x8_t &hi, bf16x8_t &lo) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        const uint16_t h = bf16_rne(x[j]);
-        const uint16_t l = bf16_rne(x[j] - bf16_val(h));
-        hi[j] = __builtin_bit_cast(__bf16, h);
-        lo[j] = __builtin_bit_cast(__bf16, l);
+        const __bf16 h = (__bf16)x[j];
+        hi[j] = h;
+        lo[j] = (__bf16)(x[j] - (float)h);
     }
+}
+
+// The LDS transposing read: within each group of 16 lanes, lane i receives
+// element i % 4 of the 4-element (8-byte) chunks addressed by lanes i/4 + 4j,
+// j = 0..3.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+__device__ inline uint2 lds_read_tr16(const uint16_t *p) {
+    const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_t *)(p));
+    return __builtin_bit_cast(uint2, v);
 }
 
 __device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -499,7 +502,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     constexpr int KC = D / 32;           // 32-long chunks of the head dimension (scores)
     constexpr int KL = F8 ? KC / 2 : KC; // 16-byte K loads per lane per 16-token half
     constexpr int MB = D / 16;           // 16-dim blocks of the output
-    constexpr int VP = D + 4;            // LDS row pitch of the V tile, in halves
+    constexpr int VP = D + 16;           // LDS row pitch of the V tile, in halves (rows 8 banks apart)
     constexpr int VL = kMfmaTile * D / EPL / kWave;  // 16-byte V loads per lane per tile
     static_assert(VL * kWave * EPL == kMfmaTile * D, "V tile split over the wave");
     // first dim of the lane's 8-long slice of contraction chunk c (Q and K alike)
@@ -556,7 +559,36 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     // load i -> token (lane + 64 i) / (D/EPL), 16 bytes at dim
     // EPL * ((lane + 64 i) % (D/EPL)).  Tokens past the split read the split's
     // last token again (in bounds) and are masked out of the softmax.
+    // A full tile takes the fast path: each half's page base is wave-uniform
+    // (scalar registers) and every lane adds a fixed 32-bit offset: for K
+    // r16 * D + chunk_dim(0, kg) (later chunks by immediate offsets), for V
+    // load i lane * EPL plus a constant (load i covers 64 / (D/EPL) whole
+    // tokens, all in one half).  Only the split's last tile clamps per lane.
+    const uint32_t k_lane = (uint32_t)(r16 * D + chunk_dim(0, kg));
+    const uint32_t v_lane = (uint32_t)(lane * EPL);
+    constexpr int TPI = kWave / (D / EPL);  // tokens per V load instruction
+    static_assert(16 % TPI == 0, "a V load stays inside one half");
+    auto half_base = [&](int s0) -> int64_t {  // s0: first token of a half, wave-uniform, < n_tok
+        const int64_t pg = __builtin_amdgcn_readfirstlane(sm_pg[s0 / BT]);
+        return (pg * n_kv_heads + g) * (int64_t)BT * D + (int64_t)(s0 % BT) * D;
+    };
     auto load_tile = [&](int t, uint4 (&kb)[2][KL], uint4 (&vb)[VL]) {
+        if (t * kMfmaTile + kMfmaTile <= n_tok) {
+            int64_t base[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) base[h] = half_base(t * kMfmaTile + 16 * h);
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int c = 0; c < KL; ++c)
+                    kb[h][c] = load_stream16(k_pool + base[h] + k_lane + (chunk_dim(c * EPL / 8, 0) - chunk_dim(0, 0)));
+#pragma unroll
+            for (int i = 0; i < VL; ++i) {
+                const int h = i * TPI / 16;
+                vb[i] = load_stream16(v_pool + base[h] + v_lane + (i * TPI - 16 * h) * D);
+            }
+            return;
+        }
         const T *kbase[2], *vbase[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -618,10 +650,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
                 st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qlo[c], st, 0, 0, 0);
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int s = t * kMfmaTile + 16 * h + 4 * kg + i;
-                sc[4 * h + i] = s < n_tok ? st[i] : -INFINITY;
-            }
+            for (int i = 0; i < 4; ++i) sc[4 * h + i] = st[i];
+        }
+        if (t * kMfmaTile + kMfmaTile > n_tok) {  // the split's last tile: mask tokens past its end
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (t * kMfmaTile + 16 * (j / 4) + 4 * kg + j % 4 >= n_tok) sc[j] = -INFINITY;
         }
         // online softmax of row r16 (replicated over the 4 kg lanes)
         float cm = sc[0];
@@ -632,7 +666,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         const float mn = fmaxf(mrun, cm);
         const float msafe = mn == -INFINITY ? 0.f : mn;
         if (__any(mn > mrun)) {
-            const float alpha = exp2f(mrun - msafe);
+            const float alpha = exp2_hw(mrun - msafe);
             lpart *= alpha;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) acc[mb] *= alpha;
@@ -641,20 +675,21 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         float pr[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            pr[j] = exp2f(sc[j] - msafe);
+            pr[j] = exp2_hw(sc[j] - msafe);
             lpart += pr[j];
         }
         bf16x8_t phi, plo;
         split_bf16x8(pr, phi, plo);
-        // output: A = V^T (dims 16mb + r16, tokens 16(j/4) + 4kg + j%4 from LDS)
+        // output: A = V^T, lane (r16, kg) needs dims 16mb + r16 of tokens
+        // 16(j/4) + 4kg + j%4.  Lane r16 of group kg addresses token
+        // 4kg + r16/4 (+16 for the second read), dims 16mb + 4(r16 % 4) .. +3;
+        // the transposing read then hands each lane its dim of the 4 tokens.
+        const uint16_t *vrow = my_v + (4 * kg + r16 / 4) * VP + 4 * (r16 % 4);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-            bf16x8_t va;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int x = 16 * (j / 4) + 4 * kg + (j % 4);
-                va[j] = __builtin_bit_cast(__bf16, my_v[x * VP + 16 * mb + r16]);
-            }
+            const uint2 a = lds_read_tr16(vrow + 16 * mb);
+            const uint2 b = lds_read_tr16(vrow + 16 * VP + 16 * mb);
+            const bf16x8_t va = as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
             acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[mb], 0, 0, 0);
             acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[mb], 0, 0, 0);
         }

@@ -88,6 +88,11 @@ __device__ inline void rope_cos_sin(int64_t pos, double f, float *c, float *s) {
 
 __device__ inline float shfl_xor_f(float v, int mask) { return __shfl_xor(v, mask, kWave); }
 
+// 2^x by the hardware instruction alone (v_exp_f32).  Results below 2^-126
+// come out as zero; the softmax weights that use it are relative to a running
+// maximum, so such a weight is negligible next to the maximum's own weight 1.
+__device__ inline float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // DPP lane patterns inside one 16-lane row (gfx9 encodings; row_newbcast is gfx90a+).
 constexpr int kDppRowMirror = 0x140;      // lane i <- lane 15-i
 constexpr int kDppRowHalfMirror = 0x141;  // lane i <- lane 7-i within each half row
