@@ -96,9 +96,10 @@ kvmem_status make_select_plan(const kvmem_geom *g, int32_t n_layers, int32_t n_q
         return fail(KVMEM_ERR_SHAPE, "mode %d is not a kvmem_reduce value", mode);
     const int group = g->n_q_heads / g->n_kv_heads;
     const int rows = group * n_q;
-    if (!pow2(rows) || rows > 16)
+    if (!((pow2(rows) && rows <= 16) || (rows % 16 == 0 && rows <= kvmem::kRowsMaxPerHead)))
         return fail(KVMEM_ERR_UNSUPPORTED,
-                    "G * n_q_tokens = %d: scoring needs a power of two <= 16", rows);
+                    "G * n_q_tokens = %d: scoring needs a power of two <= 16 or a multiple of 16 <= %d", rows,
+                    kvmem::kRowsMaxPerHead);
     int32_t k_eff = 0, n_view = 0;
     st = plan_view(g, n_blocks, n_sink, n_recent, model_ctx, gpu_kv, &k_eff, &n_view);
     if (st != KVMEM_OK) return st;

@@ -27,6 +27,13 @@ __host__ __device__ inline int64_t index_layer_floats(int64_t n_blocks, int n_kv
 // ---- select ------------------------------------------------------------
 // Index tiles scored by one workgroup of the logit kernel (one per wave).
 constexpr int kScoreTilesPerGroup = 4;
+// More than 16 query rows per KV head (a recall point's prefill query): one
+// workgroup per index tile runs every row of its (layer, KV head) in chunks of
+// 16 on the matrix cores; the block relevance then sums the rows in
+// partitions of about kReduceRowsPerPart rows (at most kReduceMaxParts).
+constexpr int kRowsMaxPerHead = 4096;
+constexpr int kReduceRowsPerPart = 512;
+constexpr int kReduceMaxParts = 64;
 // Selection: candidates are handled in chunks of kSelChunk (one workgroup
 // each); the key histogram has kSelBins bins (bits 30..19 of the score key),
 // the second level inside the pivot bin kSelBins2 (bits 18..8).
@@ -42,7 +49,9 @@ struct SelectPlan {
     int n_rows;   // n_layers * n_q * n_q_heads
     int tile_lo;     // first index tile holding a candidate
     int n_tiles;     // index tiles holding candidates
+    int tiles_per_part;  // index tiles per logit workgroup
     int n_parts;     // logit workgroups along the candidates = partial stats per row
+    int n_rsplit;    // row partitions of the block-relevance sum (1: one pass)
     int cand_stride; // row stride of logits and score rows (n_cand rounded up to 64)
     int n_chunks;    // ceil(n_cand / kSelChunk)
     // byte offsets into the workspace
@@ -52,6 +61,7 @@ struct SelectPlan {
     size_t off_rmax;    // float  [n_rows]
     size_t off_rinvz;   // double [n_rows]
     size_t off_r32;     // float  [n_sel][cand_stride]
+    size_t off_rpart;   // double [n_rsplit][n_sel][cand_stride] partial relevance (n_rsplit > 1)
     // uint32 [n_sel][kSelBins] key histogram, [n_sel][kSelBins2] pivot-bin
     // histogram, [n_sel] pivot-bin key count (all zeroed by the score stats)
     size_t off_hist;
@@ -65,7 +75,13 @@ inline void plan_select_layout(SelectPlan &p) {
     p.n_rows = p.n_layers * p.n_q * p.n_q_heads;
     p.tile_lo = p.n_sink / kIndexTile;
     p.n_tiles = (int)index_tiles(p.n_blocks - p.n_recent) - p.tile_lo;
-    p.n_parts = (p.n_tiles + kScoreTilesPerGroup - 1) / kScoreTilesPerGroup;
+    p.tiles_per_part = p.rows_per_head > 16 ? 1 : kScoreTilesPerGroup;
+    p.n_parts = (p.n_tiles + p.tiles_per_part - 1) / p.tiles_per_part;
+    {
+        const int nr = p.mode == 0 ? p.n_rows : p.n_q * p.group;  // logit rows behind one relevance value
+        int parts = nr / kReduceRowsPerPart;
+        p.n_rsplit = parts < 2 ? 1 : (parts > kReduceMaxParts ? kReduceMaxParts : parts);
+    }
     p.cand_stride = (p.n_cand + 63) / 64 * 64;
     p.n_chunks = (p.n_cand + kSelChunk - 1) / kSelChunk;
     size_t o = 0;
@@ -75,6 +91,7 @@ inline void plan_select_layout(SelectPlan &p) {
     p.off_rmax = o;   o = align_up(o + sizeof(float) * (size_t)p.n_rows);
     p.off_rinvz = o;  o = align_up(o + sizeof(double) * (size_t)p.n_rows);
     p.off_r32 = o;    o = align_up(o + sizeof(float) * (size_t)p.n_sel * p.cand_stride);
+    p.off_rpart = o;  o = align_up(o + (p.n_rsplit > 1 ? sizeof(double) * (size_t)p.n_rsplit * p.n_sel * p.cand_stride : 0));
     p.off_hist = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * kSelHistWords);
     p.off_ctrl = o;   o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * 8);
     p.off_above = o;  o = align_up(o + sizeof(uint32_t) * (size_t)p.n_sel * p.n_chunks);

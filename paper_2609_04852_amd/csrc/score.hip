@@ -210,6 +210,98 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     }
 }
 
+// More than 16 query rows per KV head (a recall point: the prefill's query
+// tokens x the group's heads).  The scoring is then a dense contraction,
+// S = Q index^T, run on the fp64 matrix cores for the same reason as above.
+// One workgroup per (index tile, KV head, layer): the tile's 64 x D floats are
+// staged in LDS once and serve every row of that (layer, KV head); each wave
+// takes 16-row chunks in turn.  Per chunk and 16-dim slice c, lane l (r16 =
+// l % 16, kg = l / 16) holds the 4 dims 16c + 4kg .. of query row r16 (A
+// operand) and of block 16gb + r16 (B operand, gb = 0..3); contraction slot kg
+// stands for those dims on both sides.  Lane l receives the logits of rows
+// kg + 4i of the chunk for block 16gb + r16, so every row's 64 logits sit in
+// the 16 lanes of one kg group, which also reduce its (max, sum of exp).
+template <int D>
+__global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
+    const float *__restrict__ q, const float *__restrict__ index, int n_blocks, int n_kv_heads,
+    int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
+    int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
+    double *__restrict__ tsum) {
+    constexpr int NW = kScoreThreads / kWave, NC = D / 16;
+    __shared__ float4 sm_idx[D / 4][kIndexTile];  // the tile in its stored layout: [j4][block]
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r16 = lane % 16, kg = lane / 16;
+    const int g = blockIdx.y, l = blockIdx.z;
+    const int tile = tile_lo + blockIdx.x;
+    {
+        const int64_t tiles_per_layer = index_tiles(n_blocks);
+        const float4 *src = reinterpret_cast<const float4 *>(
+            index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) * (int64_t)(D / 4) * (kIndexTile * 4));
+        for (int i = threadIdx.x; i < (D / 4) * kIndexTile; i += kScoreThreads)
+            sm_idx[i / kIndexTile][i % kIndexTile] = src[i];
+    }
+    __syncthreads();
+    const int64_t b0 = (int64_t)tile * kIndexTile - n_sink;  // candidate of the tile's first block
+    // candidates of this lane's 4 blocks (16gb + r16) that are in C
+    bool cok[4];
+#pragma unroll
+    for (int gb = 0; gb < 4; ++gb) cok[gb] = b0 + 16 * gb + r16 >= 0 && b0 + 16 * gb + r16 < n_cand;
+    const int rows = n_q * group;
+    for (int chunk = wave; chunk < rows / 16; chunk += NW) {
+        // A operand: query row chunk*16 + r16 of (layer l, KV head g)
+        const int r = chunk * 16 + r16;
+        const int64_t qrow = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
+        f64x4_t st[4];
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll 2
+        for (int c = 0; c < NC; ++c) {
+            const float4 a = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
+            const float av[4] = {a.x, a.y, a.z, a.w};
+            float4 bv[4];
+#pragma unroll
+            for (int gb = 0; gb < 4; ++gb) bv[gb] = sm_idx[4 * c + kg][16 * gb + r16];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int gb = 0; gb < 4; ++gb) {
+                    const float be = e == 0 ? bv[gb].x : e == 1 ? bv[gb].y : e == 2 ? bv[gb].z : bv[gb].w;
+                    st[gb] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)av[e], (double)be, st[gb], 0, 0, 0);
+                }
+        }
+        // lane: rows kg + 4i of the chunk, blocks 16gb + r16
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int rr = chunk * 16 + kg + 4 * i;
+            const int64_t row = ((int64_t)l * n_q + rr / group) * n_q_heads + g * group + rr % group;
+            float sv[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int gb = 0; gb < 4; ++gb) {
+                sv[gb] = (float)(st[gb][i] * (double)scale);
+                if (cok[gb]) {
+                    logits[row * cand_stride + b0 + 16 * gb + r16] = sv[gb];
+                    mx = fmaxf(mx, sv[gb]);
+                }
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, shfl_xor_f(mx, o));
+            double e = 0.0;
+            if (mx != -INFINITY) {
+#pragma unroll
+                for (int gb = 0; gb < 4; ++gb)
+                    if (cok[gb]) e += (double)expf(sv[gb] - mx);
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) e += __shfl_xor(e, o, kWave);
+            if (r16 == 0) {
+                tmax[row * n_parts + blockIdx.x] = mx;
+                tsum[row * n_parts + blockIdx.x] = e;
+            }
+        }
+    }
+}
+
 __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float *__restrict__ tmax,
                                                                     const double *__restrict__ tsum,
                                                                     int n_parts, float *__restrict__ rmax,
@@ -259,11 +351,67 @@ __global__ __launch_bounds__(kScoreThreads) void score_stats_kernel(const float 
 constexpr int kReduceCols = kScoreThreads / 4;  // float4 columns per workgroup
 constexpr int kReduceCands = 4 * kReduceCols;
 
+// With many logit rows behind each relevance value (a recall point), the sum
+// (or max) over rows is split: workgroup (candidate chunk, selection row, part)
+// covers rows [part * nr / n_part, (part + 1) * nr / n_part) exactly as
+// score_reduce does all of them, and leaves its fp64 partial in rpart;
+// score_reduce then combines the parts in order.
+__global__ __launch_bounds__(kScoreThreads) void score_reduce_part_kernel(
+    const float *__restrict__ logits, const float *__restrict__ rmax, const double *__restrict__ rinvz,
+    int n_layers, int n_q, int n_q_heads, int n_kv_heads, int group, int n_cand, int64_t cand_stride, int mode,
+    int n_sel, double *__restrict__ rpart) {
+    __shared__ double sm_acc[4][kReduceCols][4];
+    const int sel = blockIdx.y, part = blockIdx.z, n_part = gridDim.z;
+    const int col = threadIdx.x % kReduceCols, rs = threadIdx.x / kReduceCols;
+    const int c0 = blockIdx.x * kReduceCands + 4 * col;
+    const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
+    const int i0 = (int)((int64_t)part * nr / n_part), i1 = (int)((int64_t)(part + 1) * nr / n_part);
+    const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    if (c0 < n_cand) {
+#pragma unroll 8
+        for (int i = i0 + rs; i < i1; i += 4) {
+            const int64_t row = mode == 0 ? (int64_t)i
+                                          : ((int64_t)l * n_q + i / group) * n_q_heads + g * group + i % group;
+            const float4 x = *reinterpret_cast<const float4 *>(logits + row * cand_stride + c0);
+            const float mx = rmax[row];
+            const double iz = rinvz[row];
+            const float xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const double pr = (double)expf(xs[e] - mx) * iz;
+                if (mode == 0) acc[e] += pr;
+                else acc[e] = pr > acc[e] ? pr : acc[e];
+            }
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sm_acc[rs][col][e] = acc[e];
+    __syncthreads();
+    if (rs == 0 && c0 < n_cand) {
+        double out[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            double a = sm_acc[0][col][e];
+#pragma unroll
+            for (int k = 1; k < 4; ++k) {
+                const double b = sm_acc[k][col][e];
+                a = mode == 0 ? a + b : (b > a ? b : a);
+            }
+            out[e] = a;
+        }
+        double *dst = rpart + ((int64_t)part * n_sel + sel) * cand_stride + c0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = out[e];
+    }
+}
+
 __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     const float *__restrict__ logits, const float *__restrict__ rmax,
     const double *__restrict__ rinvz, int n_layers, int n_q, int n_q_heads, int n_kv_heads,
     int group, int n_blocks, int n_sink, int n_cand, int64_t cand_stride, int mode,
-    float *__restrict__ r32, float *__restrict__ scores, uint32_t *__restrict__ hist) {
+    float *__restrict__ r32, float *__restrict__ scores, uint32_t *__restrict__ hist,
+    const double *__restrict__ rpart, int n_rsplit) {
     __shared__ uint32_t lh[kSelBins];
     __shared__ double sm_acc[4][kReduceCols][4];
     const int sel = blockIdx.y;
@@ -274,7 +422,16 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
     const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
     double acc[4] = {0.0, 0.0, 0.0, 0.0};
-    if (c0 < n_cand) {
+    if (c0 < n_cand && rpart) {
+        // the row partitions' partials, in order (slice 0 only)
+        if (rs == 0) {
+            for (int k = 0; k < n_rsplit; ++k) {
+                const double *src = rpart + ((int64_t)k * gridDim.y + sel) * cand_stride + c0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[e] = mode == 0 ? acc[e] + src[e] : (src[e] > acc[e] ? src[e] : acc[e]);
+            }
+        }
+    } else if (c0 < n_cand) {
 #pragma unroll 8
         for (int i = rs; i < nr; i += 4) {
             const int64_t row = mode == 0 ? (int64_t)i
@@ -356,7 +513,14 @@ hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *ind
                                tsum);
             return hipGetLastError();
         }
-        default: return hipErrorInvalidValue;
+        default: {
+            if (p.rows_per_head % 16 != 0 || p.tiles_per_part != 1) return hipErrorInvalidValue;
+            dim3 grid(p.n_tiles, p.n_kv_heads, p.n_layers);
+            hipLaunchKernelGGL((score_logits_rows_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
+                               p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
+                               (int64_t)p.cand_stride, p.tile_lo, p.n_parts, scale, logits, tmax, tsum);
+            return hipGetLastError();
+        }
     }
 }
 
@@ -383,9 +547,18 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
     }
     // at least one workgroup per row, which also marks the reserved blocks' scores
     const int n_red = (p.n_cand + kReduceCands - 1) / kReduceCands;
+    double *rpart = nullptr;
+    if (p.n_rsplit > 1 && p.n_cand > 0) {
+        rpart = reinterpret_cast<double *>(ws + p.off_rpart);
+        hipLaunchKernelGGL(score_reduce_part_kernel, dim3(n_red, p.n_sel, p.n_rsplit), dim3(kScoreThreads), 0,
+                           stream, logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
+                           p.n_cand, (int64_t)p.cand_stride, p.mode, p.n_sel, rpart);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(score_reduce_kernel, dim3(n_red > 0 ? n_red : 1, p.n_sel), dim3(kScoreThreads), 0, stream,
                        logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
-                       p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist);
+                       p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist, rpart,
+                       p.n_rsplit);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk(p, block_to_page, view_blocks, view_pages, ws, stream);
 }

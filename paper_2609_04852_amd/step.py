@@ -110,3 +110,50 @@ class LayerState:
         """One decode step of this layer: select, then attention over the view."""
         self.select(q_layer, with_scores=False, stream=stream)
         return self.attend(q_layer[0], stream=stream)
+
+
+class RecallState:
+    """A recall point (Sec. 4.2, Eq. 10): the Mean-K indexes of several layers in
+    one buffer and one selection over all of them from a multi-token query."""
+
+    def __init__(self, cfg: Config, k_pools: list, block_to_page: np.ndarray, device="cuda",
+                 budget_tokens: int | None = None, n_q: int | None = None):
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.geom = geom_of(cfg)
+        g = self.geom
+        self.n_layers = len(k_pools)
+        self.n_q = cfg.n_q if n_q is None else n_q
+        self.budget = cfg.budget_tokens if budget_tokens is None else budget_tokens
+        self.mode = mode_of(cfg)
+        self.block_to_page = torch.from_numpy(np.ascontiguousarray(block_to_page, np.int32)).to(self.device)
+        self.n_blocks = int(block_to_page.shape[0])
+        self.layer_floats = K.kvmem_index_bytes(g, self.n_blocks) // 4
+        self.index = torch.empty(self.n_layers * self.layer_floats, dtype=torch.float32, device=self.device)
+        self.k_pools = [pool_to_device(k, self.device) for k in k_pools]
+        self.k_eff, self.n_view = K.kvmem_plan_view(g, self.n_blocks, cfg.sink_blocks, cfg.n_recent,
+                                                    self.budget, self.budget)
+        self.n_sel = 1 if self.mode == K.KVMEM_REDUCE_MEAN_ALL else self.n_layers * g.n_kv_heads
+        self.view_blocks = torch.empty((self.n_sel, self.n_view), dtype=torch.int32, device=self.device)
+        self.view_pages = torch.empty_like(self.view_blocks)
+        self.scores = torch.empty((self.n_sel, self.n_blocks), dtype=torch.float32, device=self.device)
+        ws = K.kvmem_select_workspace_bytes(g, self.n_layers, self.n_q, self.n_blocks, cfg.sink_blocks,
+                                            cfg.n_recent, self.mode)
+        self.select_ws = torch.empty(ws, dtype=torch.uint8, device=self.device)
+
+    def layer_index(self, l: int) -> torch.Tensor:
+        return self.index[l * self.layer_floats:(l + 1) * self.layer_floats]
+
+    def build_index(self, stream=None):
+        for l, kp in enumerate(self.k_pools):
+            K.kvmem_build_index(self.geom, kp, self.block_to_page, 0, self.n_blocks, self.layer_index(l), stream)
+
+    def index_rows(self, l: int) -> np.ndarray:
+        g = self.geom
+        return K.index_rows(self.layer_index(l).cpu().numpy(), self.n_blocks, g.n_kv_heads, g.head_dim).copy()
+
+    def select(self, q: torch.Tensor, with_scores: bool = True, stream=None) -> int:
+        """q [L][n_q][Hq][d]: the recall point's query over every layer."""
+        return K.kvmem_select(self.geom, q, self.index, self.n_blocks, self.cfg.sink_blocks, self.cfg.n_recent,
+                              self.budget, self.budget, self.mode, 0.0, self.block_to_page, self.view_blocks,
+                              self.view_pages, self.select_ws, self.scores if with_scores else None, stream)

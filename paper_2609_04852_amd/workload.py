@@ -122,6 +122,14 @@ CONFIGS = {
                       4, 8, 32, 128, "bf16", 1048576, 64, 8192, 0, 262144, 4, MAX_GROUP, 0,
                       "mixture", 4, 3968),
 }
+# A recall point (Sec. 4.2, Eq. 10 as printed; the Table 4 setting): after the
+# prefill of a new agent step, its 128 query tokens select one working set for
+# all layers and heads; the view then stays fixed for the step's decode.
+CONFIGS["1m_recall"] = Config(
+    "1m_recall", "recall point: 4 layers x 1,048,576-token history, 8x4 GQA, d128, bf16 K/V, 32-token "
+    "blocks, 128-token query (the step's prefill), one selection for all layers and heads (Eq. 10), "
+    "budget 65,536 tokens (top-k 1,792 + 8,192 recent)", 4, 8, 32, 128, "bf16", 1048576, 32, 8192, 0, 65536,
+    128, MEAN_ALL, 256, "offset", 5, 1792)
 # The FP8 variants of the 1M-token workloads (same draws, stored as E4M3 codes).
 CONFIGS["1m_fp8"] = CONFIGS["1m"].replace(
     name="1m_fp8", kv_dtype="fp8", kv_scale=float(np.float32(8 / 448)),

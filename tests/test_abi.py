@@ -134,7 +134,8 @@ def test_select_validation(L):
     assert _select(L, g, n_recent=4096, ws_bytes=big) == "KVMEM_ERR_SHAPE"
     assert _select(L, g, mode=5, ws_bytes=big) == "KVMEM_ERR_SHAPE"
     assert _select(L, g, n_q=3, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 12
-    assert _select(L, g, n_q=8, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 32
+    assert _select(L, g, n_q=9, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 36
+    assert _select(L, g, n_q=1028, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 4112 > 4096
     assert _select(L, g, n_blocks=65536 + 1024, n_recent=512, model=10**9, gpu=10**9,
                    ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"
     assert _select(L, g, n_layers=0, ws_bytes=big) == "KVMEM_ERR_SHAPE"
