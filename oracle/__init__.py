@@ -14,6 +14,8 @@ Entry points and the passages they follow:
   view_attention    Sec. 4.4 / Sec. 5.3: attention through the view's page table
   masked_dense_attention   the same attention as dense attention with the
                     non-view blocks masked out
+  working_set.WorkingSet   Eq. 11, Eq. 12 (Sec. 4.4): the working-set delta and
+                    the physical loads of a recall point over a bounded page pool
   decode_e4m3, decode_fp8  FP8 K/V (the KV-cache precision of Sec. 6's
                     platforms): OCP E4M3 codes to fp64, times the pool's scale;
                     the entry points above take the decoded pool as float64

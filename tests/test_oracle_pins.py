@@ -573,3 +573,108 @@ class TestFp8:
             o_ref, l_ref = sdpa(q[0, h][None], kk[None], vv_[None], 0.2)
             np.testing.assert_allclose(out[0, h], o_ref[0], rtol=0, atol=1e-12)
             assert lse[0, h] == pytest.approx(float(l_ref[0]), abs=1e-12)
+
+
+# ---- Working-set update at a recall point (Sec. 4.4, Eq. 11, Eq. 12) ------
+from oracle.working_set import WorkingSet  # noqa: E402
+
+
+def ws_snapshot(ws):
+    return {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in vars(ws).items()}
+
+
+class TestWorkingSet:
+    def random_views(self, seed, m, steps, lo, hi):
+        r = rng(seed)
+        out, prev = [], None
+        for _ in range(steps):
+            n = int(r.integers(lo, hi + 1))
+            if prev is not None and r.random() < 0.6:  # overlap with the previous working set
+                keep = r.choice(prev, size=min(len(prev), n // 2), replace=False)
+                rest = r.choice(np.setdiff1d(np.arange(m), keep), size=n - len(keep), replace=False)
+                v = np.sort(np.concatenate([keep, rest]))
+            else:
+                v = np.sort(r.choice(m, size=n, replace=False))
+            out.append(v)
+            prev = v
+        return out
+
+    def test_delta_sets_and_physical_loads(self):
+        m, p = 60, 25
+        ws = WorkingSet(m, p)
+        w_prev = set()
+        for t, view in enumerate(self.random_views(1, m, 40, 3, 20)):
+            before = ws_snapshot(ws)
+            g_prev = {b for b in range(m) if before["block_page"][b] >= 0}
+            out = ws.update(t, view, 0, 16, 3)
+            w = set(view.tolist())
+            r_t, l_t, e_t = w & w_prev, w - w_prev, w_prev - w          # Eq. 11
+            l_phys = w - g_prev                                        # Eq. 12
+            c = out["counts"]
+            assert (c[0], c[1], c[2], c[3], c[4]) == (len(w), len(r_t), len(l_t), len(e_t), len(l_phys))
+            assert r_t | l_t == w and not (r_t & l_t)
+            # every selected block is resident, one page each, and hits kept their pages
+            pages = out["exec_pages"]
+            assert len(set(pages.tolist())) == len(w) and (pages >= 0).all() and (pages < p).all()
+            for b, pg in zip(view, pages):
+                assert ws.block_page[b] == pg and ws.page_block[pg] == b
+                if b in g_prev:
+                    assert pg == before["block_page"][b]
+            # the bijection between resident blocks and occupied pages
+            res = {b: int(ws.block_page[b]) for b in range(m) if ws.block_page[b] >= 0}
+            assert sorted(res.values()) == sorted(int(q) for q in np.nonzero(ws.page_block >= 0)[0])
+            assert all(ws.page_block[q] == b for b, q in res.items())
+            # loads only for L_phys, into pages that held no block of W_t
+            built = {bb for (_, bb, _, _) in out["build"]}
+            assert l_phys <= built
+            w_prev = w
+
+    def test_pages_taken_in_clock_order(self):
+        m, p = 40, 12
+        ws = WorkingSet(m, p)
+        out = ws.update(0, np.arange(0, 10), 0, 16, 3)          # an empty pool fills from page 0
+        assert out["exec_pages"].tolist() == list(range(10)) and ws.hand == 10
+        out = ws.update(1, np.array([2, 3, 20, 21, 22, 23]), 0, 16, 3)
+        # hits 2, 3 keep pages 2, 3; the four misses take pages 10, 11, 0, 1 (from the hand,
+        # skipping nothing: pages 0 and 1 held blocks 0 and 1, which leave the pool)
+        assert out["exec_pages"].tolist() == [2, 3, 10, 11, 0, 1]
+        assert ws.hand == 2 and out["counts"][7] == 2
+        assert ws.block_page[0] == -1 and ws.block_page[1] == -1 and ws.block_page[4] == 4
+
+    def test_unchanged_working_set_moves_nothing(self):
+        ws = WorkingSet(100, 50)
+        v = np.array([3, 17, 40, 41, 99])
+        ws.update(0, v, 128, 32, 2)
+        out = ws.update(1, v, 128, 32, 2)
+        assert out["counts"].tolist() == [5, 5, 0, 0, 0, 0, 0, 0] and not out["build"] and not out["delta"]
+
+    def test_delta_bound_then_rebuild(self):
+        ws = WorkingSet(10, 10)
+        v = np.array([1, 5])
+        ws.update(0, v, 0, 16, 2)
+        kinds = []
+        for t in range(1, 8):
+            out = ws.update(t, v, 16 * t, 16, 2)                   # the view shifts by one block per step
+            kinds.append((len(out["delta"]), out["counts"][6]))
+            assert all(s == 16 for (_, _, s) in out["delta"])
+        # two delta re-encodings, then a rebuild from raw K, and so on
+        assert kinds == [(2, 0), (2, 0), (0, 2), (2, 0), (2, 0), (0, 2), (2, 0)]
+
+    def test_key_contents_follow_positions(self):
+        # play the builds and deltas on fp64 pages with the oracle's RoPE: after any
+        # sequence the page of view block i holds RoPE(raw K, first_position + i*Bt + t)
+        m, p, bt, d = 30, 14, 4, 8
+        raw = rng(5).standard_normal((m, 1, bt, d))
+        pool = np.zeros((p, 1, bt, d))
+        ws = WorkingSet(m, p)
+        views = self.random_views(6, m, 25, 2, 10)
+        for t, view in enumerate(views):
+            first = int(rng(100 + t).integers(0, 500))
+            out = ws.update(t, view, first, bt, 3)
+            for (i, b, pg, pos) in out["build"]:
+                pool[pg] = oracle.rope(raw[b], pos + np.arange(bt)[None, :], 1e4)
+            for (i, pg, s) in out["delta"]:
+                pool[pg] = oracle.rope(pool[pg], np.full((1, bt), s), 1e4)
+            for i, (b, pg) in enumerate(zip(view, out["exec_pages"])):
+                want = oracle.rope(raw[b], first + i * bt + np.arange(bt)[None, :], 1e4)
+                np.testing.assert_allclose(pool[pg], want, atol=1e-10)
