@@ -18,6 +18,10 @@
  *   kvmem_build_index_rope, kvmem_materialize, kvmem_rerope
  *                      position handling: index from RoPE-encoded keys,
  *                      re-encoding of selected blocks at compact positions
+ *   kvmem_working_set_reset, kvmem_working_set_workspace_bytes,
+ *   kvmem_working_set_update
+ *                      a recall point's working-set delta (Eq. 11, Eq. 12)
+ *                      over a bounded execution page pool with page reuse
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -188,6 +192,66 @@ kvmem_status kvmem_materialize(const kvmem_geom *geom, double rope_base, const v
  * quantise K again). */
 kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool, int64_t n_pages,
                           const int32_t *pages, const int64_t *delta_positions, int32_t n_list, void *stream);
+
+/* ---- Working-set update at a recall point (Sec. 4.4 "Retrieval-Aware
+ * Hierarchical Reuse", Eq. 11, Eq. 12) --------------------------------------
+ * The selected blocks of a recall point (the working set W_t) are placed in a
+ * bounded execution pool of P pages, reusing the pages of blocks that are still
+ * resident from earlier recalls (the GPU set G).  With W_{t-1} the previous
+ * recall's working set:
+ *   R_t = W_t & W_{t-1}, L_t = W_t - W_{t-1}, E_t = W_{t-1} - W_t   (Eq. 11)
+ *   L_t^physical = W_t - G_{t-1}                                    (Eq. 12)
+ * Only L_t^physical is loaded: its raw K is re-encoded at the block's compact
+ * position and V copied (as kvmem_materialize).  A resident block keeps its page
+ * and V; if its compact position moved, its K is re-encoded in place by the
+ * difference (as kvmem_rerope) while the page has had fewer than max_deltas
+ * such steps since its K was last built from raw K, else it is rebuilt from raw
+ * K.  The paper leaves two choices open; this library takes:
+ *   - view block i (view_blocks ascending) sits at first_position + i * Bt;
+ *   - the pages for L_t^physical are the pages holding no block of W_t, taken in
+ *     clock order from a hand (hand, hand + 1, ... mod P), one per incoming block
+ *     in view order; the hand then moves past the last page taken.  A taken
+ *     page's previous block leaves G.
+ * The repository view is a set of caller-owned device arrays: */
+typedef struct {
+    int32_t n_blocks;          /* M, history blocks */
+    int32_t n_pages;           /* P, pages of the execution pool (<= 2^22) */
+    int32_t *block_page;       /* dev [M] execution page of each block, -1 if not resident */
+    int32_t *block_last_step;  /* dev [M] last recall step that selected the block, -1 never */
+    int32_t *page_block;       /* dev [P] block held by each page, -1 if empty */
+    int64_t *page_pos;         /* dev [P] position the page's K is encoded at (its first token) */
+    int32_t *page_deltas;      /* dev [P] delta re-encodings since the page's K was built from raw K */
+    int32_t *header;           /* dev [8] previous step, |W| at that step, clock hand */
+} kvmem_working_set;
+
+/* Empty pool: every block non-resident and never selected, hand at page 0. */
+kvmem_status kvmem_working_set_reset(const kvmem_working_set *ws, void *stream);
+
+/* Workspace bytes of kvmem_working_set_update for views of up to n_view blocks. */
+size_t kvmem_working_set_workspace_bytes(int32_t n_view, int32_t n_pages);
+
+/* One recall point: steps must increase from call to call (W_{t-1} is the set
+ * of the previous call).
+ *   view_blocks    dev int32 [n_view], ascending distinct block ids (a kvmem_select
+ *                  row); ids outside [0, M) are ignored (counted, page -1)
+ *   block_to_page  dev int32 [M] page of each block in raw_k_pool / v_pool
+ *   raw_k_pool     dev [n_src_pages][Hkv][Bt][d] position-independent K
+ *   v_pool         dev [n_src_pages][Hkv][Bt][d]
+ *   k_exec_pool, v_exec_pool  dev [P][Hkv][Bt][d] the execution pool (updated)
+ *   exec_pages     dev int32 [n_view] out: execution page of each view block
+ *                  (the page table kvmem_sparse_attn reads over the execution pool)
+ *   counts         dev int32 [16] out: |W_t|, |R_t|, |L_t|, |E_t|, |L_t^physical|,
+ *                  delta re-encodings, rebuilds (delta bound reached), resident
+ *                  blocks evicted, ignored ids
+ * Requires n_view <= P, max_deltas >= 0, f32 or bf16 pools (FP8 pools return
+ * KVMEM_ERR_UNSUPPORTED: re-encoding would quantise K again), and a valid
+ * rope_base.  Calls that share the working-set arrays must not overlap. */
+kvmem_status kvmem_working_set_update(const kvmem_geom *geom, double rope_base, const kvmem_working_set *ws,
+                                      int32_t step, const int32_t *view_blocks, int32_t n_view,
+                                      int64_t first_position, int32_t max_deltas, const int32_t *block_to_page,
+                                      const void *raw_k_pool, const void *v_pool, int64_t n_src_pages,
+                                      void *k_exec_pool, void *v_exec_pool, int32_t *exec_pages, int32_t *counts,
+                                      void *workspace, size_t workspace_bytes, void *stream);
 
 /* View plan (Eq. 5, Eq. 7; host only, no HIP call).  With the active budget
  * B_a = min(model_ctx_tokens, gpu_kv_tokens) and the mandatory context of

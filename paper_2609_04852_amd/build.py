@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libkvmem.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["kvmem_api.cpp", "build_index.hip", "score.hip", "topk.hip", "attn.hip", "rope.hip"]
+SOURCES = ["kvmem_api.cpp", "build_index.hip", "score.hip", "topk.hip", "attn.hip", "rope.hip", "working_set.hip"]
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

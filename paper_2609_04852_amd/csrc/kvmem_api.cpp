@@ -280,6 +280,79 @@ kvmem_status kvmem_rerope(const kvmem_geom *geom, double rope_base, void *k_pool
                       "rerope launch");
 }
 
+namespace {
+kvmem_status ws_state(const kvmem_working_set *ws, kvmem::WorkingSetState &s) {
+    if (!ws) return fail(KVMEM_ERR_NULL, "working set is NULL");
+    if (ws->n_blocks <= 0 || ws->n_pages <= 0 || ws->n_pages > kvmem::kWsMaxPages)
+        return fail(KVMEM_ERR_SHAPE, "working set needs n_blocks > 0 and 0 < n_pages <= %d (got %d, %d)",
+                    kvmem::kWsMaxPages, ws->n_blocks, ws->n_pages);
+    if (!ws->block_page || !ws->block_last_step || !ws->page_block || !ws->page_pos || !ws->page_deltas ||
+        !ws->header)
+        return fail(KVMEM_ERR_NULL, "every working-set array must be non-NULL");
+    if (!aligned16(ws->block_page) || !aligned16(ws->block_last_step) || !aligned16(ws->page_block) ||
+        !aligned16(ws->page_pos) || !aligned16(ws->page_deltas) || !aligned16(ws->header))
+        return fail(KVMEM_ERR_ALIGN, "working-set arrays must be 16-byte aligned");
+    s = kvmem::WorkingSetState{ws->n_blocks, ws->n_pages, ws->block_page, ws->block_last_step, ws->page_block,
+                               ws->page_pos, ws->page_deltas, ws->header};
+    return KVMEM_OK;
+}
+}  // namespace
+
+kvmem_status kvmem_working_set_reset(const kvmem_working_set *ws, void *stream) {
+    kvmem::WorkingSetState s;
+    kvmem_status st = ws_state(ws, s);
+    if (st != KVMEM_OK) return st;
+    return hip_status(kvmem::launch_ws_reset(s, static_cast<hipStream_t>(stream)), "working_set_reset launch");
+}
+
+size_t kvmem_working_set_workspace_bytes(int32_t n_view, int32_t n_pages) {
+    if (n_view < 0 || n_pages <= 0 || n_pages > kvmem::kWsMaxPages || n_view > n_pages) {
+        fail(KVMEM_ERR_SHAPE, "need 0 <= n_view <= n_pages <= %d (got %d, %d)", kvmem::kWsMaxPages, n_view, n_pages);
+        return 0;
+    }
+    ok();
+    return kvmem::ws_scratch_bytes(n_view, n_pages);
+}
+
+kvmem_status kvmem_working_set_update(const kvmem_geom *geom, double rope_base, const kvmem_working_set *ws,
+                                      int32_t step, const int32_t *view_blocks, int32_t n_view,
+                                      int64_t first_position, int32_t max_deltas, const int32_t *block_to_page,
+                                      const void *raw_k_pool, const void *v_pool, int64_t n_src_pages,
+                                      void *k_exec_pool, void *v_exec_pool, int32_t *exec_pages, int32_t *counts,
+                                      void *workspace, size_t workspace_bytes, void *stream) {
+    kvmem_status st = check_geom(geom);
+    if (st != KVMEM_OK) return st;
+    if ((st = no_fp8(geom, "kvmem_working_set_update")) != KVMEM_OK) return st;
+    kvmem::WorkingSetState s;
+    if ((st = ws_state(ws, s)) != KVMEM_OK) return st;
+    if (!(rope_base > 1.0) || !std::isfinite(rope_base))
+        return fail(KVMEM_ERR_SHAPE, "rope_base %g must be a finite value above 1", rope_base);
+    if (step < 0 || n_view < 0 || n_view > ws->n_pages || max_deltas < 0)
+        return fail(KVMEM_ERR_SHAPE, "need step >= 0, 0 <= n_view <= n_pages (%d) and max_deltas >= 0 "
+                    "(got %d, %d, %d)", ws->n_pages, step, n_view, max_deltas);
+    if (n_src_pages <= 0) return fail(KVMEM_ERR_SHAPE, "n_src_pages must be positive");
+    if (!view_blocks || !block_to_page || !raw_k_pool || !v_pool || !k_exec_pool || !v_exec_pool || !exec_pages ||
+        !counts)
+        return fail(KVMEM_ERR_NULL, "view, block table, pools, exec_pages and counts must be non-NULL");
+    if (!aligned16(view_blocks) || !aligned16(block_to_page) || !aligned16(raw_k_pool) || !aligned16(v_pool) ||
+        !aligned16(k_exec_pool) || !aligned16(v_exec_pool) || !aligned16(exec_pages) || !aligned16(counts))
+        return fail(KVMEM_ERR_ALIGN, "device arrays must be 16-byte aligned");
+    const size_t need = kvmem::ws_scratch_bytes(n_view, ws->n_pages);
+    if (!workspace || workspace_bytes < need)
+        return fail(KVMEM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes,
+                    need);
+    kvmem::WsScratch w;
+    kvmem::ws_scratch_bytes(n_view, ws->n_pages, &w, static_cast<char *>(workspace));
+    kvmem::RopeFreqs fr;
+    kvmem::rope_freqs(rope_base, geom->head_dim, fr);
+    return hip_status(kvmem::launch_ws_update(s, w, geom->kv_dtype, geom->head_dim, geom->n_kv_heads,
+                                              geom->block_tokens, fr, step, view_blocks, n_view, first_position,
+                                              max_deltas, block_to_page, raw_k_pool, v_pool, n_src_pages,
+                                              k_exec_pool, v_exec_pool, exec_pages, counts,
+                                              static_cast<hipStream_t>(stream)),
+                      "working_set_update launch");
+}
+
 kvmem_status kvmem_plan_view(const kvmem_geom *geom, int32_t n_blocks, int32_t n_sink_blocks,
                              int32_t n_recent_blocks, int64_t model_ctx_tokens,
                              int64_t gpu_kv_tokens, int32_t *k_eff, int32_t *n_view) {

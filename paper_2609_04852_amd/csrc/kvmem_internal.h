@@ -135,8 +135,51 @@ inline void rope_freqs(double base, int head_dim, RopeFreqs &fr) {
     for (int j = 0; j < 64; ++j) fr.f[j] = j < head_dim / 2 ? pow(base, -2.0 * (double)j / (double)head_dim) : 0.0;
 }
 
+// ---- working-set update (Eq. 11, Eq. 12) ---------------------------------
+constexpr int kWsHeaderWords = 8;   // [0] previous step (-1: none), [1] |W| then, [2] clock hand
+constexpr int kWsMaxPages = 1 << 22;
+
+struct WorkingSetState {  // caller-owned device arrays (see kvmem_working_set in kvmem.h)
+    int32_t n_blocks, n_pages;
+    int32_t *block_page, *block_last_step, *page_block;
+    int64_t *page_pos;
+    int32_t *page_deltas, *header;
+};
+
+struct WsScratch {  // per-update scratch carved from the caller's workspace
+    int32_t *kept;       // [P] page holds a selected block
+    int32_t *kind;       // [n_view] unchanged / delta / rebuild / load / invalid
+    int32_t *retained;   // [n_view] selected at the previous recall too
+    int32_t *rank;       // [n_view] rank inside its kind
+    int32_t *taken;      // [n_view] pages for the loads, in order
+    int32_t *build_src, *build_dst, *delta_page;  // [n_view] lists
+    int32_t *lists;      // [16] build length, delta length, loads in the build list
+    int64_t *build_pos, *delta_shift;            // [n_view]
+};
+
+inline size_t ws_scratch_bytes(int n_view, int n_pages, WsScratch *w = nullptr, char *base = nullptr) {
+    size_t o = 0;
+    auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return base + at; };
+    int32_t *kept = (int32_t *)take(4 * (size_t)n_pages);
+    int32_t *kind = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *retained = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *rank = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *taken = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *build_src = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *build_dst = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *delta_page = (int32_t *)take(4 * (size_t)n_view);
+    int32_t *lists = (int32_t *)take(4 * 16);
+    int64_t *build_pos = (int64_t *)take(8 * (size_t)n_view);
+    int64_t *delta_shift = (int64_t *)take(8 * (size_t)n_view);
+    if (w) *w = WsScratch{kept, kind, retained, rank, taken, build_src, build_dst, delta_page, lists, build_pos,
+                          delta_shift};
+    return o;
+}
+
 // ---- launchers (return the launch status) -------------------------------
 // kv_dtype: 0 fp32, 1 bf16 bits, 2 FP8 E4M3 codes (scaled by k_scale, v_scale).
+// materialize / rope_delta: with n_dev set, the first *n_dev of the n list
+// entries are processed (the count is known on the device only).
 // block_pos / fr are used only when rope is set: the keys carry RoPE at
 // positions block_pos[b] + t (block_pos NULL: b * block_tokens + t).
 hipError_t launch_build_index(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens,
@@ -149,11 +192,19 @@ hipError_t launch_materialize(int kv_dtype, int head_dim, int n_kv_heads, int bl
                               const RopeFreqs &fr, const void *raw_k, const void *v_src,
                               int64_t n_src_pages, const int32_t *src_pages, const int64_t *positions,
                               const int32_t *dst_pages, int32_t n, void *k_dst, void *v_dst,
-                              int64_t n_dst_pages, hipStream_t stream);
+                              int64_t n_dst_pages, hipStream_t stream, const int32_t *n_dev = nullptr);
 
 hipError_t launch_rope_delta(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens, const RopeFreqs &fr,
                              void *k_pool, int64_t n_pages, const int32_t *pages, const int64_t *delta,
-                             int32_t n, hipStream_t stream);
+                             int32_t n, hipStream_t stream, const int32_t *n_dev = nullptr);
+
+hipError_t launch_ws_reset(const WorkingSetState &s, hipStream_t stream);
+
+hipError_t launch_ws_update(const WorkingSetState &s, const WsScratch &w, int kv_dtype, int head_dim, int n_kv_heads,
+                            int block_tokens, const RopeFreqs &fr, int step, const int32_t *view, int n_view,
+                            int64_t first_pos, int max_deltas, const int32_t *block_to_page, const void *raw_k,
+                            const void *v_src, int64_t n_src_pages, void *k_exec, void *v_exec,
+                            int32_t *exec_pages, int32_t *counts, hipStream_t stream);
 
 hipError_t launch_topk(const SelectPlan &p, const int32_t *block_to_page, int32_t *view_blocks,
                        int32_t *view_pages, char *workspace, hipStream_t stream);

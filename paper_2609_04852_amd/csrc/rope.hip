@@ -85,11 +85,12 @@ __global__ __launch_bounds__(kRopeThreads) void rope_materialize_kernel(
     const T *__restrict__ raw_k, const T *__restrict__ v_src, int64_t n_src_pages,
     const int32_t *__restrict__ src_pages, const int64_t *__restrict__ positions,
     const int32_t *__restrict__ dst_pages, T *__restrict__ k_dst, T *__restrict__ v_dst,
-    int64_t n_dst_pages, int n_kv_heads, int block_tokens, RopeFreqs fr) {
+    int64_t n_dst_pages, int n_kv_heads, int block_tokens, RopeFreqs fr, const int32_t *__restrict__ n_dev) {
     using L = Lanes<T>;
     constexpr int VEC = L::VEC, HL = D / 2 / VEC;  // lanes per half row
     __shared__ float2 cs[kMaxBt * (D / 2)];        // (cos, sin) per (token, pair), shared by the heads
     const int i = blockIdx.x;
+    if (n_dev && i >= *n_dev) return;  // the list's length is known on the device only
     const int64_t src = src_pages[i], dst = dst_pages[i];
     if (dst < 0 || dst >= n_dst_pages) return;  // nowhere to write
     const bool src_ok = src >= 0 && src < n_src_pages;
@@ -131,10 +132,12 @@ __global__ __launch_bounds__(kRopeThreads) void rope_materialize_kernel(
 template <typename T, int D>
 __global__ __launch_bounds__(kRopeThreads) void rope_delta_kernel(
     T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ pages,
-    const int64_t *__restrict__ delta, int n_kv_heads, int block_tokens, RopeFreqs fr) {
+    const int64_t *__restrict__ delta, int n_kv_heads, int block_tokens, RopeFreqs fr,
+    const int32_t *__restrict__ n_dev) {
     using L = Lanes<T>;
     constexpr int VEC = L::VEC, HL = D / 2 / VEC;
     __shared__ float2 cs[D / 2];  // every token of the page turns by the same angles
+    if (n_dev && (int)blockIdx.x >= *n_dev) return;
     const int64_t page = pages[blockIdx.x];
     if (page < 0 || page >= n_pages) return;
     const int64_t dp = delta[blockIdx.x];
@@ -163,29 +166,32 @@ template <int D>
 hipError_t materialize_d(int kv_dtype, const void *raw_k, const void *v_src, int64_t n_src_pages,
                          const int32_t *src_pages, const int64_t *positions, const int32_t *dst_pages,
                          int32_t n, void *k_dst, void *v_dst, int64_t n_dst_pages, int n_kv_heads,
-                         int block_tokens, const RopeFreqs &fr, hipStream_t stream) {
+                         int block_tokens, const RopeFreqs &fr, hipStream_t stream, const int32_t *n_dev) {
     if (kv_dtype == 1)
         hipLaunchKernelGGL((rope_materialize_kernel<uint16_t, D>), dim3(n), dim3(kRopeThreads), 0, stream,
                            static_cast<const uint16_t *>(raw_k), static_cast<const uint16_t *>(v_src),
                            n_src_pages, src_pages, positions, dst_pages, static_cast<uint16_t *>(k_dst),
-                           static_cast<uint16_t *>(v_dst), n_dst_pages, n_kv_heads, block_tokens, fr);
+                           static_cast<uint16_t *>(v_dst), n_dst_pages, n_kv_heads, block_tokens, fr, n_dev);
     else
         hipLaunchKernelGGL((rope_materialize_kernel<float, D>), dim3(n), dim3(kRopeThreads), 0, stream,
                            static_cast<const float *>(raw_k), static_cast<const float *>(v_src), n_src_pages,
                            src_pages, positions, dst_pages, static_cast<float *>(k_dst),
-                           static_cast<float *>(v_dst), n_dst_pages, n_kv_heads, block_tokens, fr);
+                           static_cast<float *>(v_dst), n_dst_pages, n_kv_heads, block_tokens, fr, n_dev);
     return hipGetLastError();
 }
 
 template <int D>
 hipError_t delta_d(int kv_dtype, void *k_pool, int64_t n_pages, const int32_t *pages, const int64_t *delta,
-                   int32_t n, int n_kv_heads, int block_tokens, const RopeFreqs &fr, hipStream_t stream) {
+                   int32_t n, int n_kv_heads, int block_tokens, const RopeFreqs &fr, hipStream_t stream,
+                   const int32_t *n_dev) {
     if (kv_dtype == 1)
         hipLaunchKernelGGL((rope_delta_kernel<uint16_t, D>), dim3(n), dim3(kRopeThreads), 0, stream,
-                           static_cast<uint16_t *>(k_pool), n_pages, pages, delta, n_kv_heads, block_tokens, fr);
+                           static_cast<uint16_t *>(k_pool), n_pages, pages, delta, n_kv_heads, block_tokens, fr,
+                           n_dev);
     else
         hipLaunchKernelGGL((rope_delta_kernel<float, D>), dim3(n), dim3(kRopeThreads), 0, stream,
-                           static_cast<float *>(k_pool), n_pages, pages, delta, n_kv_heads, block_tokens, fr);
+                           static_cast<float *>(k_pool), n_pages, pages, delta, n_kv_heads, block_tokens, fr,
+                           n_dev);
     return hipGetLastError();
 }
 
@@ -195,23 +201,23 @@ hipError_t launch_materialize(int kv_dtype, int head_dim, int n_kv_heads, int bl
                               const RopeFreqs &fr, const void *raw_k, const void *v_src,
                               int64_t n_src_pages, const int32_t *src_pages, const int64_t *positions,
                               const int32_t *dst_pages, int32_t n, void *k_dst, void *v_dst,
-                              int64_t n_dst_pages, hipStream_t stream) {
+                              int64_t n_dst_pages, hipStream_t stream, const int32_t *n_dev) {
     if (n == 0) return hipSuccess;
     return head_dim == 128
                ? materialize_d<128>(kv_dtype, raw_k, v_src, n_src_pages, src_pages, positions, dst_pages, n,
-                                    k_dst, v_dst, n_dst_pages, n_kv_heads, block_tokens, fr, stream)
+                                    k_dst, v_dst, n_dst_pages, n_kv_heads, block_tokens, fr, stream, n_dev)
                : materialize_d<64>(kv_dtype, raw_k, v_src, n_src_pages, src_pages, positions, dst_pages, n,
-                                   k_dst, v_dst, n_dst_pages, n_kv_heads, block_tokens, fr, stream);
+                                   k_dst, v_dst, n_dst_pages, n_kv_heads, block_tokens, fr, stream, n_dev);
 }
 
 hipError_t launch_rope_delta(int kv_dtype, int head_dim, int n_kv_heads, int block_tokens, const RopeFreqs &fr,
                              void *k_pool, int64_t n_pages, const int32_t *pages, const int64_t *delta,
-                             int32_t n, hipStream_t stream) {
+                             int32_t n, hipStream_t stream, const int32_t *n_dev) {
     if (n == 0) return hipSuccess;
     return head_dim == 128 ? delta_d<128>(kv_dtype, k_pool, n_pages, pages, delta, n, n_kv_heads, block_tokens,
-                                          fr, stream)
+                                          fr, stream, n_dev)
                            : delta_d<64>(kv_dtype, k_pool, n_pages, pages, delta, n, n_kv_heads, block_tokens,
-                                         fr, stream);
+                                         fr, stream, n_dev);
 }
 
 }  // namespace kvmem

@@ -56,6 +56,13 @@ class Geom:
                           self.kv_dtype, self.k_scale, self.v_scale)
 
 
+class kvmem_working_set(ctypes.Structure):
+    _fields_ = [("n_blocks", ctypes.c_int32), ("n_pages", ctypes.c_int32),
+                ("block_page", ctypes.c_void_p), ("block_last_step", ctypes.c_void_p),
+                ("page_block", ctypes.c_void_p), ("page_pos", ctypes.c_void_p),
+                ("page_deltas", ctypes.c_void_p), ("header", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -85,8 +92,14 @@ def lib() -> ctypes.CDLL:
     L.kvmem_build_index_rope.argtypes = [G, P, i64, P, P, dbl, i32, i32, P, P]
     L.kvmem_materialize.argtypes = [G, dbl, P, P, i64, P, P, P, i32, P, P, i64, P]
     L.kvmem_rerope.argtypes = [G, dbl, P, i64, P, P, i32, P]
+    W = ctypes.POINTER(kvmem_working_set)
+    L.kvmem_working_set_reset.argtypes = [W, P]
+    L.kvmem_working_set_workspace_bytes.argtypes = [i32, i32]
+    L.kvmem_working_set_workspace_bytes.restype = sz
+    L.kvmem_working_set_update.argtypes = [G, dbl, W, i32, P, i32, i64, i32, P, P, P, i64, P, P, P, P, P, sz, P]
     for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_sparse_attn",
-                 "kvmem_build_index_rope", "kvmem_materialize", "kvmem_rerope"):
+                 "kvmem_build_index_rope", "kvmem_materialize", "kvmem_rerope", "kvmem_working_set_reset",
+                 "kvmem_working_set_update"):
         getattr(L, name).restype = ctypes.c_int
     L.kvmem_last_error.argtypes = []
     L.kvmem_last_error.restype = ctypes.c_char_p
@@ -316,3 +329,59 @@ def kvmem_rerope(geom: Geom, rope_base: float, k_pool: torch.Tensor, pages: torc
         raise ValueError("pages and delta_positions must have the same length")
     _check(lib().kvmem_rerope(ctypes.byref(geom.c()), float(rope_base), _ptr(k_pool), k_pool.shape[0],
                               _ptr(pages), _ptr(delta_positions), pages.numel(), _stream(stream)))
+
+
+class WorkingSetArrays:
+    """The repository view of an execution pool of n_pages pages (kvmem_working_set):
+    caller-owned device arrays, emptied by reset()."""
+
+    def __init__(self, n_blocks: int, n_pages: int, device="cuda"):
+        dev = torch.device(device)
+        self.n_blocks, self.n_pages = int(n_blocks), int(n_pages)
+        self.block_page = torch.empty(n_blocks, dtype=torch.int32, device=dev)
+        self.block_last_step = torch.empty(n_blocks, dtype=torch.int32, device=dev)
+        self.page_block = torch.empty(n_pages, dtype=torch.int32, device=dev)
+        self.page_pos = torch.empty(n_pages, dtype=torch.int64, device=dev)
+        self.page_deltas = torch.empty(n_pages, dtype=torch.int32, device=dev)
+        self.header = torch.empty(8, dtype=torch.int32, device=dev)
+
+    def c(self) -> kvmem_working_set:
+        return kvmem_working_set(self.n_blocks, self.n_pages, self.block_page.data_ptr(),
+                                 self.block_last_step.data_ptr(), self.page_block.data_ptr(),
+                                 self.page_pos.data_ptr(), self.page_deltas.data_ptr(), self.header.data_ptr())
+
+    def reset(self, stream=None):
+        _check(lib().kvmem_working_set_reset(ctypes.byref(self.c()), _stream(stream)))
+
+
+def kvmem_working_set_workspace_bytes(n_view: int, n_pages: int) -> int:
+    n = lib().kvmem_working_set_workspace_bytes(n_view, n_pages)
+    if n == 0:
+        raise KvmemError(-2, kvmem_last_error())
+    return n
+
+
+def kvmem_working_set_update(geom: Geom, rope_base: float, ws: WorkingSetArrays, step: int,
+                             view_blocks: torch.Tensor, first_position: int, max_deltas: int,
+                             block_to_page: torch.Tensor, raw_k_pool: torch.Tensor, v_pool: torch.Tensor,
+                             k_exec_pool: torch.Tensor, v_exec_pool: torch.Tensor, exec_pages: torch.Tensor,
+                             counts: torch.Tensor, workspace: torch.Tensor, stream=None):
+    """One recall point's working-set update (Eq. 11, Eq. 12); see kvmem.h."""
+    for t, name in ((view_blocks, "view_blocks"), (block_to_page, "block_to_page"), (exec_pages, "exec_pages"),
+                    (counts, "counts")):
+        _need(t, torch.int32, name)
+    _need(workspace, torch.uint8, "workspace")
+    for t, name in ((raw_k_pool, "raw_k_pool"), (v_pool, "v_pool"), (k_exec_pool, "k_exec_pool"),
+                    (v_exec_pool, "v_exec_pool")):
+        if kv_dtype_of(t) != geom.kv_dtype or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous pool of geom.kv_dtype")
+    if k_exec_pool.shape[0] != ws.n_pages or v_exec_pool.shape != k_exec_pool.shape:
+        raise ValueError("the execution pools must have ws.n_pages pages")
+    n_view = view_blocks.numel()
+    if exec_pages.numel() < n_view or counts.numel() < 16:
+        raise ValueError("exec_pages needs n_view entries and counts 16")
+    _check(lib().kvmem_working_set_update(ctypes.byref(geom.c()), float(rope_base), ctypes.byref(ws.c()), step,
+                                          _ptr(view_blocks), n_view, first_position, max_deltas,
+                                          _ptr(block_to_page), _ptr(raw_k_pool), _ptr(v_pool), raw_k_pool.shape[0],
+                                          _ptr(k_exec_pool), _ptr(v_exec_pool), _ptr(exec_pages), _ptr(counts),
+                                          _ptr(workspace), workspace.numel(), _stream(stream)))

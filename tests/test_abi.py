@@ -223,3 +223,33 @@ def test_fp8_position_calls_unsupported(L):
     assert "FP8" in K.kvmem_last_error()
     # the index from encoded keys does take FP8 pools (host checks pass down to the NULL check)
     assert _status(L.kvmem_build_index_rope(g, None, 10, FAKE, None, 1e6, 0, 4, FAKE, None)) == "KVMEM_ERR_NULL"
+
+
+@no_gpu
+def test_working_set_validation(L):
+    ws = K.kvmem_working_set(100, 50, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    assert L.kvmem_working_set_workspace_bytes(60, 50) == 0   # view larger than the pool
+    assert L.kvmem_working_set_workspace_bytes(10, 50) > 0
+    g = ctypes.byref(g1())
+    big = 1 << 30
+
+    def up(**kw):
+        w = kw.get("ws", ws)
+        return _status(L.kvmem_working_set_update(
+            kw.get("g", g), kw.get("base", 1e6), ctypes.byref(w) if w is not None else None, kw.get("step", 1),
+            kw.get("view", FAKE), kw.get("n", 10), 0, kw.get("md", 2), FAKE, FAKE, FAKE, 100, FAKE, FAKE, FAKE,
+            kw.get("counts", FAKE), FAKE, kw.get("wsb", big), None))
+
+    assert up(ws=None) == "KVMEM_ERR_NULL"
+    assert up(base=0.5) == "KVMEM_ERR_SHAPE"
+    assert up(step=-1) == "KVMEM_ERR_SHAPE"
+    assert up(n=51) == "KVMEM_ERR_SHAPE"
+    assert up(md=-1) == "KVMEM_ERR_SHAPE"
+    assert up(view=None) == "KVMEM_ERR_NULL"
+    assert up(counts=MISALIGNED) == "KVMEM_ERR_ALIGN"
+    assert up(wsb=16) == "KVMEM_ERR_WORKSPACE"
+    assert up(ws=K.kvmem_working_set(100, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)) == "KVMEM_ERR_SHAPE"
+    assert up(ws=K.kvmem_working_set(100, 50, FAKE, None, FAKE, FAKE, FAKE, FAKE)) == "KVMEM_ERR_NULL"
+    fp8 = ctypes.byref(g1(kv_dtype=K.KVMEM_FP8_E4M3, k_scale=0.02, v_scale=0.02))
+    assert up(g=fp8) == "KVMEM_ERR_UNSUPPORTED"
+    assert _status(L.kvmem_working_set_reset(None, None)) == "KVMEM_ERR_NULL"
