@@ -123,6 +123,157 @@ def cpu_oracle_baseline(w, seconds):
     return n, el, oracle.num_threads()
 
 
+def recall_baseline(w, seconds):
+    """The oracle's recall point on the same workload: Eq. 10 relevance over every
+    layer and query token, the selection, and the working-set update."""
+    import oracle
+    from oracle.working_set import WorkingSet
+    cfg = w.cfg
+    index = np.stack([oracle.mean_k(k, w.block_to_page) for k in w.k_pool])
+    k = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, cfg.block_tokens, cfg.n_blocks, cfg.sink_blocks,
+                     cfg.n_recent)
+    ws = WorkingSet(cfg.n_blocks, 2 * (cfg.sink_blocks + k + cfg.n_recent))
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        rel = oracle.block_relevance(w.q[n % w.q.shape[0]], index, cfg.sink_blocks, cfg.n_recent)
+        vb, _ = oracle.select(rel, cfg.sink_blocks, cfg.n_recent, k, w.block_to_page)
+        ws.update(n, vb[0], 0, cfg.block_tokens, 8)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 4:
+            break
+    return n, el, oracle.num_threads()
+
+
+def recall_bench(args, cfg, seed):
+    """A recall point (Sec. 4.2, the Table 4 setting): kvmem_select over every layer
+    and the prefill's query tokens (Eq. 10), then kvmem_working_set_update of each
+    layer's execution pool (Eq. 11, Eq. 12: only the blocks not resident are
+    loaded, raw K re-encoded at the compact positions); the decode steps that
+    follow attend over the fixed view."""
+    import torch
+
+    from paper_2609_04852_amd import kvmem as K
+    from paper_2609_04852_amd import workload as W
+    from paper_2609_04852_amd.step import RecallState, pool_to_device
+
+    n_sets = min(args.query_sets, 4)
+    print(f"[bench] generating {cfg.name} seed={seed}", file=sys.stderr, flush=True)
+    t = time.perf_counter()
+    w = W.generate(cfg, seed, n_query_sets=n_sets)
+    print(f"[bench] generated in {time.perf_counter() - t:.1f}s; uploading", file=sys.stderr, flush=True)
+    dev = torch.device("cuda", 0)
+    rs = RecallState(cfg, w.k_pool, w.block_to_page, dev)
+    g, L = rs.geom, cfg.n_layers
+    n_view, P = rs.n_view, 2 * rs.n_view
+    v_pools = [pool_to_device(v, dev) for v in w.v_pool]
+    shape = (P,) + tuple(rs.k_pools[0].shape[1:])
+    k_exec = [torch.zeros(shape, dtype=rs.k_pools[0].dtype, device=dev) for _ in range(L)]
+    v_exec = [torch.zeros_like(k_exec[0]) for _ in range(L)]
+    states = [K.WorkingSetArrays(cfg.n_blocks, P, dev) for _ in range(L)]
+    for s_ in states:
+        s_.reset()
+    exec_pages = [torch.empty((1, n_view), dtype=torch.int32, device=dev) for _ in range(L)]
+    counts = [torch.zeros(16, dtype=torch.int32, device=dev) for _ in range(L)]
+    wsp = torch.empty(K.kvmem_working_set_workspace_bytes(n_view, P), dtype=torch.uint8, device=dev)
+    qdev = torch.from_numpy(w.q).to(dev)                      # [sets][L][n_q][Hq][d]
+    qdec = qdev[:, :, :1].contiguous()                        # one decode token per layer
+    aws = torch.empty(K.kvmem_sparse_attn_workspace_bytes(g, 1, 1, n_view), dtype=torch.uint8, device=dev)
+    out = torch.empty((1, g.n_q_heads, g.head_dim), dtype=torch.float32, device=dev)
+    lse = torch.empty((1, g.n_q_heads), dtype=torch.float32, device=dev)
+    rs.build_index()
+    torch.cuda.synchronize()
+    rope_base, max_deltas = 1e6, 8
+
+    def recall(t, qs, ev=None):
+        if ev:
+            ev[0].record()
+        rs.select(qdev[qs], with_scores=False)
+        if ev:
+            ev[1].record()
+        for l in range(L):
+            K.kvmem_working_set_update(g, rope_base, states[l], t, rs.view_blocks[0], 0, max_deltas,
+                                       rs.block_to_page, rs.k_pools[l], v_pools[l], k_exec[l], v_exec[l],
+                                       exec_pages[l][0], counts[l], wsp)
+        if ev:
+            ev[2].record()
+
+    def decode(qs):
+        for l in range(L):
+            K.kvmem_sparse_attn(g, qdec[qs, l], k_exec[l], v_exec[l], exec_pages[l], 1, n_view,
+                                cfg.block_tokens, 0.0, out, aws, lse)
+
+    recall(0, 0)  # fills the pools (every block loaded)
+    torch.cuda.synchronize()
+    n_rec = max(4, min(args.steps // 10, 40))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_rec)]
+    cnt = np.zeros((n_rec, 8), np.int64)
+    print(f"[bench] timing {n_rec} recall points", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(n_rec):
+        recall(i + 1, (i + 1) % n_sets, evs[i])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / n_rec
+    sel = np.array([a.elapsed_time(b) for a, b, c in evs])
+    upd = np.array([b.elapsed_time(c) for a, b, c in evs])
+    tot = np.array([a.elapsed_time(c) for a, b, c in evs])
+    last_counts = counts[0][:8].cpu().numpy().tolist()
+    # decode over the fixed view
+    for i in range(3):
+        decode(i % n_sets)
+    torch.cuda.synchronize()
+    n_dec = max(10, args.steps)
+    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    d0.record()
+    for i in range(n_dec):
+        decode(i % n_sets)
+    d1.record()
+    torch.cuda.synchronize()
+    dec_ms = d0.elapsed_time(d1) / n_dec
+    # work of one recall: logits on the fp64 matrix cores, and the bytes moved
+    rows = L * cfg.n_q * cfg.n_q_heads
+    flops = 2.0 * rows * cfg.n_candidates * cfg.head_dim
+    page_bytes = cfg.n_kv_heads * cfg.block_tokens * cfg.head_dim * cfg.elem_bytes
+    sel_ms = float(np.median(sel))
+    cpu = None
+    if args.cpu_seconds > 0:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        n, el, cores = recall_baseline(w, args.cpu_seconds)
+        cpu = {"value": round(n / el, 5), "unit": "recalls/s", "cores": cores, "kind": "oracle",
+               "sample": f"{n} full recall points of the same workload (fp64 Eq. 10 over every layer and "
+                         f"query token, selection, working-set update; index built beforehand), {el:.1f}s"}
+    res = {
+        "metric": "recall points/s (Eq. 10 over every layer and query token + top-k + working-set update) "
+                  "@1M-token history",
+        "value": round(1000.0 / float(np.median(tot)), 3),
+        "unit": "recalls/s",
+        "n_gpus": 1,
+        "steps": n_rec,
+        "warmup": 1,
+        "ms_per_step": round(float(np.median(tot)), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": cfg.description, "name": cfg.name, "layers": L, "query_tokens": cfg.n_q,
+                   "history_tokens": cfg.history_tokens, "block_tokens": cfg.block_tokens, "view_blocks": n_view,
+                   "execution_pool_pages": P, "max_delta_reencodings": max_deltas, "seed": seed},
+        "recall": {"select_ms_p50": round(sel_ms, 4), "working_set_update_ms_p50": round(float(np.median(upd)), 4),
+                   "wall_ms_per_recall": round(wall_ms, 4),
+                   "last_counts_W_R_L_E_Lphys_delta_rebuild_evicted": last_counts,
+                   "logit_flops": flops,
+                   "select_TFLOPs_fp64": round(flops / (sel_ms * 1e-3) / 1e12, 2),
+                   "fp64_matrix_peak_TFLOPs": 78.6},
+        "decode_over_view": {"ms_per_step": round(dec_ms, 4), "steps_per_s": round(1000.0 / dec_ms, 1),
+                             "GBps": round(L * n_view * page_bytes * 2 / (dec_ms * 1e-3) / 1e9, 1)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -143,6 +294,8 @@ def main():
     K.lib()  # fail loudly if the HIP library is not built
     cfg = W.CONFIGS[args.config]
     seed = cfg.seed if args.seed is None else args.seed
+    if cfg.n_q > 16:  # a recall-point workload
+        return recall_bench(args, cfg, seed)
     print(f"[bench] generating {cfg.name} seed={seed}", file=sys.stderr, flush=True)
     t = time.perf_counter()
     w = W.generate(cfg, seed, n_query_sets=args.query_sets)
