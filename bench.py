@@ -24,7 +24,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 ATTN_SOURCES = ["paper_2609_04852_amd/csrc/attn.hip", "paper_2609_04852_amd/csrc/kvmem_device.h",
                 "paper_2609_04852_amd/csrc/kvmem_internal.h"]
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "sparse_attn_1m_traffic.json")
+def traffic_file(name):
+    """The counter record of the sparse-attention call on workload `name`."""
+    return os.path.join(HERE, "profiles", f"sparse_attn_{name}_traffic.json")
 
 
 def parse():
@@ -383,8 +385,8 @@ def main():
                 "attn_ms_p10_p50_p90": [round(float(np.percentile(attn_all, p)), 5) for p in (10, 50, 90)]}
         achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
         traffic = None
-        if os.path.exists(TRAFFIC_FILE):
-            with open(TRAFFIC_FILE) as f:
+        if os.path.exists(traffic_file(cfg.name)):
+            with open(traffic_file(cfg.name)) as f:
                 tr = json.load(f)
             if tr.get("source_digest") == source_digest(ATTN_SOURCES) and tr.get("config") == cfg.name:
                 traffic = tr.get("hbm_bytes_per_launch")
