@@ -39,7 +39,9 @@ def parse():
     p.add_argument("--query-sets", type=int, default=8)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the CPU-oracle baseline sample (0 disables it)")
-    p.add_argument("--graph", action="store_true", help="replay the steps from a captured HIP graph")
+    p.add_argument("--no-graph", dest="graph", action="store_false",
+                   help="time eager launches only (by default the headline rate replays the steps from a "
+                        "captured HIP graph; the roofline always comes from the eager pass)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run 5 device-to-device copies of MIB MiB (known bytes, for scaling "
                         "rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -337,38 +339,44 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
+    # eager pass: every attention call bracketed by events (roofline, distribution)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps * cfg.n_layers)]
+    print(f"[bench] timing {args.steps} eager steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        for l, st in enumerate(layers):
+            qs = qdev[i % n_sets]
+            st.select(qs[l:l + 1], with_scores=False)
+            a, b = evs[i * cfg.n_layers + l]
+            a.record(stream)
+            st.attend(qs[l])
+            b.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    eager_ms = (t1 - t0) * 1000.0 / args.steps
+    n_steps, ms_per_step = args.steps, eager_ms
     graph = None
     if args.graph:
+        # the same steps, one per query set, captured once and replayed: every
+        # replay runs the whole selection and attention of each step again
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             for i in range(n_sets):
                 step(i)
         graph.replay()
         torch.cuda.synchronize()
-
-    # attention-call events, one pair per (step, layer)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps * cfg.n_layers)] if graph is None else []
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if graph is None:
-        for i in range(args.steps):
-            for l, st in enumerate(layers):
-                qs = qdev[i % n_sets]
-                st.select(qs[l:l + 1], with_scores=False)
-                a, b = evs[i * cfg.n_layers + l]
-                a.record(stream)
-                st.attend(qs[l])
-                b.record(stream)
-    else:
         reps = max(1, args.steps // n_sets)
+        print(f"[bench] timing {reps * n_sets} steps by graph replay", file=sys.stderr, flush=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
         for _ in range(reps):
             graph.replay()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    n_steps = args.steps if graph is None else max(1, args.steps // n_sets) * n_sets
-    ms_per_step = (t1 - t0) * 1000.0 / n_steps
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        n_steps = reps * n_sets
+        ms_per_step = (t1 - t0) * 1000.0 / n_steps
 
     sel_bytes, attn_bytes = algorithmic_bytes(cfg)
     step_bytes = cfg.n_layers * (sel_bytes + attn_bytes)
@@ -488,6 +496,7 @@ def main():
                    "view_tokens": cfg.n_view * cfg.block_tokens, "query_tokens": cfg.n_q,
                    "selection": cfg.mode, "seed": seed, "query_sets": n_sets,
                    "hip_graph": graph is not None},
+        "eager_ms_per_step": round(eager_ms, 5),
         "step_bytes": step_bytes,
         "step_GBps": round(gbps, 1),
         "step_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),

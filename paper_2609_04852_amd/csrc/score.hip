@@ -58,8 +58,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
         const int64_t tiles_per_layer = index_tiles(n_blocks);
         const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
                                        (int64_t)(D / 4) * (kIndexTile * 4) + lane * 4;
-#pragma unroll 8
-        for (int j4 = 0; j4 < D / 4; ++j4) {
+#pragma unroll
+        for (int j4 = 0; j4 < D / 4; ++j4) {  // every load of the tile in flight at once
             const float4 x = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
 #pragma unroll
             for (int r = 0; r < RH; ++r) {
