@@ -254,13 +254,22 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
         f64x4_t st[4];
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
-#pragma unroll 2
+        float4 qa[NC];  // the chunk's query slices, all in flight before the products start
+#pragma unroll
+        for (int c = 0; c < NC; ++c) qa[c] = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
+        float4 bn[4];
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb) bn[gb] = sm_idx[kg][16 * gb + r16];
+#pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const float4 a = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
-            const float av[4] = {a.x, a.y, a.z, a.w};
             float4 bv[4];
 #pragma unroll
-            for (int gb = 0; gb < 4; ++gb) bv[gb] = sm_idx[4 * c + kg][16 * gb + r16];
+            for (int gb = 0; gb < 4; ++gb) bv[gb] = bn[gb];
+            if (c + 1 < NC) {
+#pragma unroll
+                for (int gb = 0; gb < 4; ++gb) bn[gb] = sm_idx[4 * (c + 1) + kg][16 * gb + r16];
+            }
+            const float av[4] = {qa[c].x, qa[c].y, qa[c].z, qa[c].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -268,6 +277,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
                     const float be = e == 0 ? bv[gb].x : e == 1 ? bv[gb].y : e == 2 ? bv[gb].z : bv[gb].w;
                     st[gb] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)av[e], (double)be, st[gb], 0, 0, 0);
                 }
+            __builtin_amdgcn_sched_barrier(0);  // next slice's LDS reads overlap these products, no further
         }
         // lane: rows kg + 4i of the chunk, blocks 16gb + r16
 #pragma unroll
