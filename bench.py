@@ -236,6 +236,25 @@ def recall_bench(args, cfg, seed):
     d1.record()
     torch.cuda.synchronize()
     dec_ms = d0.elapsed_time(d1) / n_dec
+    # the step's prefill query replayed over the fixed view (every layer, all
+    # query tokens: K/V tiles shared through LDS by row groups)
+    aws_r = torch.empty(K.kvmem_sparse_attn_workspace_bytes(g, cfg.n_q, 1, n_view), dtype=torch.uint8, device=dev)
+    out_r = torch.empty((cfg.n_q, g.n_q_heads, g.head_dim), dtype=torch.float32, device=dev)
+    lse_r = torch.empty((cfg.n_q, g.n_q_heads), dtype=torch.float32, device=dev)
+
+    def replay(qs):
+        for l in range(L):
+            K.kvmem_sparse_attn(g, qdev[qs, l], k_exec[l], v_exec[l], exec_pages[l], 1, n_view,
+                                cfg.block_tokens, 0.0, out_r, aws_r, lse_r)
+
+    replay(0)
+    torch.cuda.synchronize()
+    d0.record()
+    for i in range(10):
+        replay(i % n_sets)
+    d1.record()
+    torch.cuda.synchronize()
+    rep_ms = d0.elapsed_time(d1) / 10
     # work of one recall: logits on the fp64 matrix cores, and the bytes moved
     rows = L * cfg.n_q * cfg.n_q_heads
     flops = 2.0 * rows * cfg.n_candidates * cfg.head_dim
@@ -273,6 +292,10 @@ def recall_bench(args, cfg, seed):
                    "fp64_matrix_peak_TFLOPs": 78.6},
         "decode_over_view": {"ms_per_step": round(dec_ms, 4), "steps_per_s": round(1000.0 / dec_ms, 1),
                              "GBps": round(L * n_view * page_bytes * 2 / (dec_ms * 1e-3) / 1e9, 1)},
+        "prefill_replay_over_view": {"query_tokens": cfg.n_q, "ms_all_layers": round(rep_ms, 4),
+                                     "bf16_TFLOPs": round(8.0 * L * cfg.n_q * cfg.n_q_heads * n_view *
+                                                          cfg.block_tokens * cfg.head_dim / (rep_ms * 1e-3) / 1e12,
+                                                          1)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

@@ -753,6 +753,196 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     }
 }
 
+// Many query rows per KV head (a step's prefill replayed over the view: e.g.
+// 128 tokens x 4 GQA heads = 512 rows).  The workgroup's NW waves each own 16
+// rows and share every 32-token K/V tile: the whole workgroup loads it once
+// into one of two LDS stages (K and V as bf16; FP8 codes widened on the way
+// in), so K/V is read from memory once per 16 NW rows instead of once per 16
+// (at 512 rows: 466 us with 4 waves, 300 with 8, 288 with 16 over a 64K view).
+// Per tile each wave runs the products of attn_mfma16 with its K operand read
+// from LDS (row pitch D + 8 halves: the 16 rows of one read sit 4 banks apart)
+// and V^T by the transposing reads; each wave keeps its rows' running softmax
+// and writes their partials itself (no merge across waves).
+// NW waves (16 rows each) share one K/V tile: 4, 8 or 16 by the row count
+template <typename T, int D, int BT, int NW>
+__global__ __launch_bounds__(NW * kWave) void attn_mfma_rows_kernel(
+    const float *__restrict__ q, const T *__restrict__ k_pool, const T *__restrict__ v_pool,
+    int64_t n_pages, const int32_t *__restrict__ view_pages, int n_sel, int n_view, int last_page_tokens,
+    int n_kv_heads, int n_q_heads, int group, int rows_total, int pages_per_split, int n_splits,
+    float qscale, float v_scale, float *__restrict__ part) {
+    constexpr bool F8 = sizeof(T) == 1;
+    constexpr int EPL = 16 / sizeof(T);               // elements per 16-byte load
+    constexpr int KC = D / 32, MB = D / 16;
+    constexpr int KP = D + 8, VP = D + 16;            // LDS row pitches, in halves
+    constexpr int UPR = D / EPL;                      // 16-byte units per token row
+    constexpr int LPT = kMfmaTile * UPR;              // units per tile, K or V
+    constexpr int NT = NW * kWave;
+    constexpr int LPL = (LPT + NT - 1) / NT;          // per thread
+    __shared__ __attribute__((aligned(16))) uint16_t sm_k[2][kMfmaTile * KP];
+    __shared__ __attribute__((aligned(16))) uint16_t sm_v[2][kMfmaTile * VP];
+    __shared__ int32_t sm_pg[kAttnMaxPages];
+    const int split = blockIdx.x, g = blockIdx.y;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r16 = lane % 16, kg = lane / 16;
+    const int row0 = blockIdx.z * (NW * kMfmaRows) + wave * kMfmaRows;
+    const int32_t *vpages = view_pages + (int64_t)(n_sel == 1 ? 0 : g) * n_view;
+    const int p_begin = split * pages_per_split;
+    const int p_end = min(n_view, p_begin + pages_per_split);
+    const int n_tok = (p_end - p_begin) * BT - (p_end == n_view ? BT - last_page_tokens : 0);
+    const int n_tiles = (n_tok + kMfmaTile - 1) / kMfmaTile;
+    bool bad = false;
+    for (int i = threadIdx.x; i < p_end - p_begin; i += NT) {
+        const int32_t pg = vpages[p_begin + i];
+        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
+        sm_pg[i] = ok ? pg : 0;  // an invalid id is never read; the split's partial becomes NaN
+        bad |= !ok;
+    }
+    const bool any_bad = __syncthreads_or(bad) != 0;
+
+    // Q^T operand of this wave's 16 rows, hi + lo bf16 (padding rows are zero)
+    bf16x8_t qhi[KC], qlo[KC];
+    {
+        const int row = min(row0 + r16, rows_total - 1), m = row / group, hh = row % group;
+        const float qs = row0 + r16 < rows_total ? qscale : 0.f;
+        const float *qp = q + ((int64_t)m * n_q_heads + g * group + hh) * D + 8 * kg;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+            const float4 a = *reinterpret_cast<const float4 *>(qp + 32 * c);
+            const float4 b = *reinterpret_cast<const float4 *>(qp + 32 * c + 4);
+            const float x[8] = {a.x * qs, a.y * qs, a.z * qs, a.w * qs, b.x * qs, b.y * qs, b.z * qs, b.w * qs};
+            split_bf16x8(x, qhi[c], qlo[c]);
+        }
+    }
+    f32x4_t acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float mrun = -INFINITY, lpart = 0.f;
+
+    // unit u of tile t: token u / UPR, EPL elements at dim EPL * (u % UPR); tokens
+    // past the split read its last token again and are masked out of the softmax
+    auto load = [&](int t, uint4 (&kr)[LPL], uint4 (&vr)[LPL]) {
+#pragma unroll
+        for (int i = 0; i < LPL; ++i) {
+            const int u = threadIdx.x + NT * i;
+            if (LPT % NT == 0 || u < LPT) {
+                const int tok = min(t * kMfmaTile + u / UPR, n_tok - 1);
+                const int64_t off = ((int64_t)sm_pg[tok / BT] * n_kv_heads + g) * (int64_t)BT * D +
+                                    (int64_t)(tok % BT) * D + EPL * (u % UPR);
+                kr[i] = load_stream16(k_pool + off);
+                vr[i] = load_stream16(v_pool + off);
+            }
+        }
+    };
+    auto put = [&](uint16_t *dst, const uint4 &x) {
+        if constexpr (F8) {
+            uint2 *d2 = reinterpret_cast<uint2 *>(dst);
+            d2[0] = fp8x4_to_bf16x4(x.x);
+            d2[1] = fp8x4_to_bf16x4(x.y);
+            d2[2] = fp8x4_to_bf16x4(x.z);
+            d2[3] = fp8x4_to_bf16x4(x.w);
+        } else {
+            *reinterpret_cast<uint4 *>(dst) = x;
+        }
+    };
+    auto stage = [&](int st, const uint4 (&kr)[LPL], const uint4 (&vr)[LPL]) {
+#pragma unroll
+        for (int i = 0; i < LPL; ++i) {
+            const int u = threadIdx.x + NT * i;
+            if (LPT % NT == 0 || u < LPT) {
+                const int x = u / UPR, col = EPL * (u % UPR);
+                put(&sm_k[st][x * KP + col], kr[i]);
+                put(&sm_v[st][x * VP + col], vr[i]);
+            }
+        }
+    };
+    auto process = [&](int t, int st) {
+        const uint16_t *kt = sm_k[st];
+        float sc[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                const bf16x8_t kk =
+                    as_bf16x8(*reinterpret_cast<const uint4 *>(kt + (16 * h + r16) * KP + 32 * c + 8 * kg));
+                s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qhi[c], s4, 0, 0, 0);
+                s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qlo[c], s4, 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sc[4 * h + i] = s4[i];
+        }
+        if (t * kMfmaTile + kMfmaTile > n_tok) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (t * kMfmaTile + 16 * (j / 4) + 4 * kg + j % 4 >= n_tok) sc[j] = -INFINITY;
+        }
+        float cm = sc[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) cm = fmaxf(cm, sc[j]);
+        cm = fmaxf(cm, shfl_xor_f(cm, 16));
+        cm = fmaxf(cm, shfl_xor_f(cm, 32));
+        const float mn = fmaxf(mrun, cm);
+        const float msafe = mn == -INFINITY ? 0.f : mn;
+        if (__any(mn > mrun)) {
+            const float alpha = exp2_hw(mrun - msafe);
+            lpart *= alpha;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) acc[mb] *= alpha;
+        }
+        mrun = mn;
+        float pr[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            pr[j] = exp2_hw(sc[j] - msafe);
+            lpart += pr[j];
+        }
+        bf16x8_t phi, plo;
+        split_bf16x8(pr, phi, plo);
+        const uint16_t *vrow = sm_v[st] + (4 * kg + r16 / 4) * VP + 4 * (r16 % 4);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const uint2 a = lds_read_tr16(vrow + 16 * mb);
+            const uint2 b = lds_read_tr16(vrow + 16 * VP + 16 * mb);
+            const bf16x8_t va = as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[mb], 0, 0, 0);
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[mb], 0, 0, 0);
+        }
+    };
+    {
+        uint4 kr[LPL], vr[LPL];
+        if (n_tiles > 0) {
+            load(0, kr, vr);
+            stage(0, kr, vr);
+        }
+        __syncthreads();
+        for (int t = 0; t < n_tiles; ++t) {
+            const int st = t & 1;
+            if (t + 1 < n_tiles) load(t + 1, kr, vr);
+            process(t, st);
+            // the other stage was last read in iteration t - 1, before the barrier
+            if (t + 1 < n_tiles) stage(st ^ 1, kr, vr);
+            __syncthreads();
+        }
+    }
+    float lrun = lpart + shfl_xor_f(lpart, 16);
+    lrun += shfl_xor_f(lrun, 32);
+    if (row0 + r16 < rows_total) {
+        float *dst = part + (((int64_t)g * n_splits + split) * rows_total + row0 + r16) * (D + kPartStride);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const float4 o = any_bad ? make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
+                                                   __builtin_nanf(""))
+                                     : make_float4(acc[mb][0] * v_scale, acc[mb][1] * v_scale, acc[mb][2] * v_scale,
+                                                   acc[mb][3] * v_scale);
+            *reinterpret_cast<float4 *>(dst + 16 * mb + 4 * kg) = o;
+        }
+        if (kg == 0) {
+            dst[D] = mrun;
+            dst[D + 1] = lrun;
+        }
+    }
+}
+
 constexpr int kCombineThreads = 256;
 
 // One workgroup per (KV head, row).  The split weights 2^(m_s - M) are formed
@@ -857,17 +1047,44 @@ hipError_t launch_mfma16(const AttnPlan &p, const float *q, const void *k_pool, 
     return hipGetLastError();
 }
 
+// rows per KV head from which K/V tiles are shared through LDS by 64-row groups
+constexpr int kRowsLds = 48;
+
+template <typename T, int D, int BT, int NW>
+hipError_t launch_mfma_rows_nw(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
+                               int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
+                               hipStream_t stream) {
+    dim3 grid(p.n_splits, p.n_kv_heads, (p.rows_per_head + NW * kMfmaRows - 1) / (NW * kMfmaRows));
+    hipLaunchKernelGGL((attn_mfma_rows_kernel<T, D, BT, NW>), grid, dim3(NW * kWave), 0, stream, q,
+                       static_cast<const T *>(k_pool), static_cast<const T *>(v_pool), n_pages, view_pages, p.n_sel,
+                       p.n_view, p.last_page_tokens, p.n_kv_heads, p.n_q_heads, p.group, p.rows_per_head,
+                       p.pages_per_split, p.n_splits, qscale, p.v_scale, part);
+    return hipGetLastError();
+}
+
+template <typename T, int D, int BT>
+hipError_t launch_mfma_rows(const AttnPlan &p, const float *q, const void *k_pool, const void *v_pool,
+                            int64_t n_pages, const int32_t *view_pages, float qscale, float *part,
+                            hipStream_t stream) {
+    if (p.rows_per_head <= 64)
+        return launch_mfma_rows_nw<T, D, BT, 4>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
+    if (p.rows_per_head <= 128)
+        return launch_mfma_rows_nw<T, D, BT, 8>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
+    return launch_mfma_rows_nw<T, D, BT, 16>(p, q, k_pool, v_pool, n_pages, view_pages, qscale, part, stream);
+}
+
 template <typename T, int D, int BT>
 hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const void *v, int64_t n_pages,
                      const int32_t *vp, float qscale, float *part, hipStream_t stream) {
     const int rows = p.rows_per_head;
     if constexpr (std::is_same<T, uint8_t>::value) {
         // FP8: always the matrix cores (rows padded to 16)
-        (void)rows;
+        if (rows >= kRowsLds) return launch_mfma_rows<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
         return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
     } else {
         if constexpr (std::is_same<T, uint16_t>::value) {
             // bf16 with 4 or more rows per KV head: matrix cores (rows padded to 16)
+            if (rows >= kRowsLds) return launch_mfma_rows<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
             if (rows >= 4) return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
         }
         if constexpr (D / Vec16<T>::N == 16) {

@@ -407,3 +407,49 @@ def test_fp8_out_of_range_pages_give_nan():
     o_ref, _ = oracle.view_attention(q[:, :8], oracle_pool(cfg, w.k_pool[0])[:, :1],
                                      oracle_pool(cfg, w.v_pool[0])[:, :1], vp[:1])
     np.testing.assert_allclose(o[:, :8], o_ref, atol=2e-2, rtol=0)
+
+
+# ---- Many query rows per KV head (a prefill replayed over the view): K/V tiles
+# shared through LDS by 64-row groups ------------------------------------------
+MANY_ROWS = [
+    # Hkv, Hq, d, Bt, dtype, n_q, pages in view, last page tokens, n_sel
+    (2, 8, 128, 16, "bf16", 128, 70, 16, 1),   # 512 rows
+    (2, 8, 128, 32, "bf16", 20, 41, 7, 2),     # 80 rows: a ragged second row group
+    (4, 16, 64, 64, "bf16", 12, 23, 33, 4),    # 48 rows, d64
+    (2, 8, 128, 16, "fp8", 32, 90, 5, 1),      # 128 rows, FP8
+    (1, 4, 64, 32, "fp8", 16, 17, 32, 1),      # 64 rows, FP8 d64
+    (2, 8, 64, 32, "fp8", 50, 33, 9, 2),       # 200 rows: 256-row groups, ragged, per-head views
+]
+
+
+@pytest.mark.parametrize("case", MANY_ROWS, ids=[f"m{i}" for i in range(len(MANY_ROWS))])
+def test_many_rows_attention(case):
+    hkv, hq, d, bt, dt, nq, nv, lpt, n_sel = case
+    cfg = W.small_config(n_kv_heads=hkv, n_q_heads=hq, head_dim=d, block_tokens=bt, kv_dtype=dt,
+                         kv_scale=float(np.float32(8 / 448)), history_tokens=200 * bt, recent_tokens=2 * bt,
+                         budget_tokens=(nv + 2) * bt, n_q=nq, mode=W.MEAN_ALL if n_sel == 1 else W.MAX_GROUP)
+    log(f"[case] many rows: Hkv={hkv} Hq={hq} d={d} Bt={bt} {dt} n_q={nq} rows/head={nq * hq // hkv} "
+        f"view={nv} last={lpt} n_sel={n_sel}")
+    w = W.generate(cfg, 51)
+    rng = np.random.default_rng(6)
+    vp = np.stack([rng.choice(cfg.n_blocks, nv, replace=False) for _ in range(n_sel)]).astype(np.int32)
+    q = np.ascontiguousarray(w.q[0, 0])
+    o_ref, l_ref = oracle.view_attention(q, oracle_pool(cfg, w.k_pool[0]), oracle_pool(cfg, w.v_pool[0]), vp,
+                                         last_page_tokens=lpt)
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page, n_q=nq)
+    out, lse = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(vp).cuda(), last_page_tokens=lpt)
+    torch.cuda.synchronize()
+    err = check_attention(out.cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, dt)
+    log(f"  max abs err out {err[0]:.2e} lse {err[1]:.2e}")
+    # an invalid page in one head's view: that head's rows become NaN, the others do not change
+    if n_sel > 1:
+        vp2 = vp.copy()
+        vp2[1, nv // 2] = cfg.n_blocks + 7
+        out2, _ = st.attend(torch.from_numpy(q).cuda(), torch.from_numpy(vp2).cuda(), last_page_tokens=lpt)
+        torch.cuda.synchronize()
+        o2 = out2.cpu().numpy()
+        g_size = hq // hkv
+        assert np.isnan(o2[:, g_size:2 * g_size]).all()
+        keep = np.ones(hq, bool)
+        keep[g_size:2 * g_size] = False
+        np.testing.assert_array_equal(o2[:, keep], out.cpu().numpy()[:, keep])
