@@ -41,7 +41,7 @@ constexpr int kSelChunk = 1024;
 constexpr int kSelBins = 4096;
 constexpr int kSelBins2 = 2048;
 constexpr int kSelHistWords = kSelBins + kSelBins2 + 1;  // per selection row, with the pivot-bin count
-constexpr int kTopkMaxCand = 1024 * 64;  // <= 64 chunks per selection row
+constexpr int kTopkMaxCand = 1 << 20;  // candidates per selection row (1,024 chunks)
 
 struct SelectPlan {
     int n_layers, n_q, n_q_heads, n_kv_heads, head_dim, group, rows_per_head;

@@ -45,8 +45,6 @@ constexpr int kDigitBits = 11;
 constexpr int kSubShift = 8;            // second-level digit: key bits 18..8
 constexpr int kWindowCap = 8192;        // sub-pivot keys kept in LDS
 constexpr int kBruteMax = kFinishThreads;  // sub-pivot sets ranked pairwise
-constexpr int kMaxChunks = kTopkMaxCand / kSelChunk;
-static_assert(kMaxChunks <= kWave && kMaxChunks <= kFinishThreads, "one lane per chunk");
 static_assert(kSelBins2 << kSubShift == 1 << 19, "second level = the bits below the first");
 
 enum { kCtrlPivot = 0, kCtrlRank = 3 };
@@ -163,7 +161,6 @@ struct FinishShared {
     uint32_t s_digit, s_krem;
     uint32_t s_thr, s_cut;
     uint32_t wcnt[kFinishThreads / kWave];  // sub-pivot keys found by each wave
-    uint32_t above[kMaxChunks];
     // sub-pivot (key, candidate), in no particular order: wave w fills
     // window[w * kWaveCap ...]
     uint2 window[kWindowCap];
@@ -276,7 +273,6 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
     const uint32_t k_in = ctrl[sel * 8 + kCtrlRank];  // rank inside the pivot bin
     const uint32_t n_b = min(*h.count, (uint32_t)n_cand);  // keys in the pivot bin (<= n_cand)
     const uint2 *row = seg + (int64_t)sel * n_chunks * kSelChunk;
-    if (tid < n_chunks) sh.above[tid] = above_cnt[sel * n_chunks + tid];
     // sub-pivot bin and the rank inside it (its barriers also publish `above`)
     uint32_t sub, above_sub;
     find_pivot<NT, kSelBins2>(h.h2, k_in, sh.scratch, sh.s_out, &sub, &above_sub);
@@ -371,7 +367,7 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
             return true;
         }, nmax, k_sub, sh, &k_rem);
         // among keys equal to thr, the k_rem lowest candidate ids: rank k_rem
-        // of (2^16 - c), which is larger for lower c (c < 2^16)
+        // of ~c, which is larger for lower c
         uint32_t n_tie = 0u;
         for (int j = 0; j < nmax; ++j) {
             uint2 it;
@@ -385,10 +381,10 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
             const uint32_t kk = exact_rank([&](int j, uint32_t *key) {
                 uint2 it;
                 if (!get_item(j, &it) || it.x != thr) return false;
-                *key = 0x10000u - it.y;
+                *key = ~it.y;
                 return true;
             }, nmax, k_rem, sh, &dummy);
-            cut = 0x10000u - kk;
+            cut = ~kk;
         }
         for (int j = 0; j < nmax; ++j) {
             uint2 it;
@@ -399,7 +395,7 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
     }
     const uint32_t thr = sh.s_thr, cut = sh.s_cut;
     // output offset of this chunk: every selection in the chunks before it
-    if (tid < chunk) before += sh.above[tid];
+    for (int i = tid; i < chunk; i += NT) before += above_cnt[(int64_t)sel * n_chunks + i];
     uint32_t base;
     block_exclusive_scan<NT>(before, sh.scratch, &base);
     // emit this chunk's selected candidates in order

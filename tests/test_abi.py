@@ -94,7 +94,7 @@ def test_workspace_queries():
     aws = K.kvmem_sparse_attn_workspace_bytes(g, 1, 1, c.n_view)
     assert aws > 0
     with pytest.raises(K.KvmemError):
-        K.kvmem_select_workspace_bytes(g, 1, 1, 70000 * 2, 0, 512, 0)  # too many candidates
+        K.kvmem_select_workspace_bytes(g, 1, 1, (1 << 20) + 1024, 0, 512, 0)  # too many candidates
     with pytest.raises(K.KvmemError):
         K.kvmem_sparse_attn_workspace_bytes(g, 1, 3, 10)  # n_sel must be 1 or Hkv
 
@@ -136,7 +136,7 @@ def test_select_validation(L):
     assert _select(L, g, n_q=3, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 12
     assert _select(L, g, n_q=9, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 36
     assert _select(L, g, n_q=1028, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 4112 > 4096
-    assert _select(L, g, n_blocks=65536 + 1024, n_recent=512, model=10**9, gpu=10**9,
+    assert _select(L, g, n_blocks=(1 << 20) + 1024, n_recent=512, model=10**9, gpu=10**9,
                    ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"
     assert _select(L, g, n_layers=0, ws_bytes=big) == "KVMEM_ERR_SHAPE"
 

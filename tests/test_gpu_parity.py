@@ -453,3 +453,44 @@ def test_many_rows_attention(case):
         keep = np.ones(hq, bool)
         keep[g_size:2 * g_size] = False
         np.testing.assert_array_equal(o2[:, keep], out.cpu().numpy()[:, keep])
+
+
+# ---- More than 65,536 candidates (histories beyond 1M tokens in 16-token
+# blocks; the Table 4 scalability range) -------------------------------------
+def test_4m_history_select():
+    cfg = W.small_config(n_kv_heads=8, n_q_heads=32, head_dim=128, block_tokens=32, kv_dtype="bf16",
+                         history_tokens=4 * 1048576, recent_tokens=8192, budget_tokens=65536, n_q=1,
+                         n_planted=128)
+    log(f"[case] 4M-token history: {cfg.n_blocks} blocks, {cfg.n_candidates} candidates")
+    w = W.generate(cfg, 61, with_values=False)
+    index_ref = oracle.mean_k(w.k_pool[0], w.block_to_page)
+    rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 0, cfg.n_recent)
+    k_eff = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, 32, cfg.n_blocks, 0, cfg.n_recent)
+    vb_ref, _ = oracle.select(rel, 0, cfg.n_recent, k_eff, w.block_to_page)
+    st = LayerState(cfg, w.k_pool[0], None, w.block_to_page)
+    st.build_index()
+    torch.cuda.synchronize()
+    assert_index_bitwise(st.index_rows(), index_ref)
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    stats = check_selection(st.view_blocks.cpu().numpy(), st.view_pages.cpu().numpy(), rel, w.block_to_page, 0,
+                            cfg.n_recent, k_eff, ref_view=vb_ref)
+    worst = check_scores(st.scores.cpu().numpy(), rel, 0, cfg.n_recent)
+    log(f"  selection ok: {stats}, worst score rel err {worst:.2e}")
+
+
+@pytest.mark.parametrize("k", [40000, 69990])
+def test_all_equal_scores_beyond_2_16(k):
+    """70,000 candidates with identical scores: the selection is the k lowest ids,
+    including ids above 2^16."""
+    m = 70000 + 5
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", m, 0, 5, 1, W.MEAN_ALL, k, planted=0)
+    log(f"[case] all scores equal, {cfg.n_candidates} candidates, k={k}")
+    w = W.generate(cfg, 62, with_values=False)
+    kp = np.broadcast_to(w.k_pool[0][:1], w.k_pool[0].shape).copy()
+    st = LayerState(cfg, kp, None, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    vb = st.view_blocks.cpu().numpy()[0]
+    assert vb.tolist() == list(range(k)) + list(range(m - 5, m))
