@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--no-graph", dest="graph", action="store_false",
                    help="time eager launches only (by default the headline rate replays the steps from a "
                         "captured HIP graph; the roofline always comes from the eager pass)")
+    p.add_argument("--sweep", default="",
+                   help="recall-point workloads only: comma-separated history sizes in tokens to time the "
+                        "recall point at (the workspace-size study of the paper's Table 4)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run 5 device-to-device copies of MIB MiB (known bytes, for scaling "
                         "rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -148,6 +151,70 @@ def recall_baseline(w, seconds):
         if el >= seconds or n >= 4:
             break
     return n, el, oracle.num_threads()
+
+
+def recall_sweep(args, cfg, seed):
+    """The recall point (selection over every layer and query token + working-set
+    update of every layer) at several history sizes, the view fixed: the
+    workspace-size study of the paper's Table 4.  Only K pools are drawn; the
+    working-set updates copy V from the K pools (the values do not change the
+    work).  One JSON line with the series."""
+    import torch
+
+    from paper_2609_04852_amd import kvmem as K
+    from paper_2609_04852_amd import workload as W
+    from paper_2609_04852_amd.step import RecallState
+
+    sizes = [int(x) for x in args.sweep.split(",") if x]
+    dev = torch.device("cuda", 0)
+    series = []
+    for h in sizes:
+        c = cfg.replace(name=f"{cfg.name}_{h}", history_tokens=h, n_planted=min(cfg.n_planted, 64))
+        print(f"[bench] sweep: {h} tokens ({c.n_blocks} blocks), generating", file=sys.stderr, flush=True)
+        w = W.generate(c, seed, n_query_sets=2, with_values=False)
+        rs = RecallState(c, w.k_pool, w.block_to_page, dev)
+        qdev = torch.from_numpy(w.q).to(dev)
+        del w
+        g, L, n_view = rs.geom, c.n_layers, rs.n_view
+        P = 2 * n_view
+        shape = (P,) + tuple(rs.k_pools[0].shape[1:])
+        k_exec = [torch.zeros(shape, dtype=rs.k_pools[0].dtype, device=dev) for _ in range(L)]
+        v_exec = [torch.zeros_like(k_exec[0]) for _ in range(L)]
+        states = [K.WorkingSetArrays(c.n_blocks, P, dev) for _ in range(L)]
+        for s_ in states:
+            s_.reset()
+        exec_pages = [torch.empty(n_view, dtype=torch.int32, device=dev) for _ in range(L)]
+        counts = torch.zeros(16, dtype=torch.int32, device=dev)
+        wsp = torch.empty(K.kvmem_working_set_workspace_bytes(n_view, P), dtype=torch.uint8, device=dev)
+        rs.build_index()
+        torch.cuda.synchronize()
+
+        def recall(t, ev):
+            ev[0].record()
+            rs.select(qdev[t % 2], with_scores=False)
+            ev[1].record()
+            for l in range(L):
+                K.kvmem_working_set_update(g, 1e6, states[l], t, rs.view_blocks[0], 0, 8, rs.block_to_page,
+                                           rs.k_pools[l], rs.k_pools[l], k_exec[l], v_exec[l], exec_pages[l],
+                                           counts, wsp)
+            ev[2].record()
+
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(6)]
+        for t in range(6):
+            recall(t, evs[t])
+        torch.cuda.synchronize()
+        sel = float(np.median([a.elapsed_time(b) for a, b, _ in evs[1:]]))
+        upd = float(np.median([b.elapsed_time(e) for _, b, e in evs[1:]]))
+        series.append({"history_tokens": h, "blocks": c.n_blocks, "select_ms": round(sel, 3),
+                       "working_set_update_ms": round(upd, 3), "recall_ms": round(sel + upd, 3)})
+        print(f"[bench] sweep: {series[-1]}", file=sys.stderr, flush=True)
+        del rs, k_exec, v_exec, states, exec_pages, wsp, qdev
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "recall-point latency vs workspace size (view fixed at "
+                                f"{cfg.budget_tokens} tokens, {cfg.n_q}-token query, {cfg.n_layers} layers)",
+                      "unit": "ms", "n_gpus": 1, "higher_is_better": False, "data": "synthetic",
+                      "config": {"workload": cfg.description, "block_tokens": cfg.block_tokens, "seed": seed},
+                      "series": series}), flush=True)
 
 
 def recall_bench(args, cfg, seed):
@@ -322,7 +389,7 @@ def main():
     cfg = W.CONFIGS[args.config]
     seed = cfg.seed if args.seed is None else args.seed
     if cfg.n_q > 16:  # a recall-point workload
-        return recall_bench(args, cfg, seed)
+        return recall_sweep(args, cfg, seed) if args.sweep else recall_bench(args, cfg, seed)
     print(f"[bench] generating {cfg.name} seed={seed}", file=sys.stderr, flush=True)
     t = time.perf_counter()
     w = W.generate(cfg, seed, n_query_sets=args.query_sets)
