@@ -1091,7 +1091,11 @@ hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const voi
             if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
             if (rows % 4 == 0) return launch_row16<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
         }
-        if (rows % 8 == 0) return launch_rh<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        // 8 rows per workgroup, except fp32 K/V with d = 128 and 64-token pages, whose
+        // 8-row kernel does not fit the registers
+        if constexpr (!(std::is_same<T, float>::value && D == 128 && BT == 64)) {
+            if (rows % 8 == 0) return launch_rh<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);
+        }
         if (rows % 4 == 0) return launch_rh<T, D, BT, 4>(p, q, k, v, n_pages, vp, qscale, part, stream);
         if (rows % 2 == 0) return launch_rh<T, D, BT, 2>(p, q, k, v, n_pages, vp, qscale, part, stream);
         return launch_rh<T, D, BT, 1>(p, q, k, v, n_pages, vp, qscale, part, stream);

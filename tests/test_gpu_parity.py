@@ -111,6 +111,8 @@ SHAPES = [
     (2, 16, 128, 16, "bf16", 700, 0, 5, 2, W.MEAN_ALL, 100),
     (4, 16, 64, 32, "bf16", 500, 1, 3, 4, W.MAX_GROUP, 60),
     (2, 8, 128, 64, "bf16", 260, 0, 2, 4, W.MAX_GROUP, 37),
+    # fp32 K/V, d128, 64-token pages, 8 rows per KV head (two 4-row workgroups)
+    (2, 16, 128, 64, "f32", 150, 0, 2, 1, W.MEAN_ALL, 20),
 ]
 
 
