@@ -37,6 +37,10 @@ def parse():
     p.add_argument("--config", default="1m", help="workload name (see workload.CONFIGS)")
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--query-sets", type=int, default=8)
+    p.add_argument("--replicas", type=int, default=None,
+                   help="copies of the pools and index that consecutive steps rotate over, so that a small "
+                        "workload streams from HBM and not from the 256 MB Infinity Cache (default: enough "
+                        "copies for 2 GiB, at most 64; 1 for workloads of 2 GiB or more)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the CPU-oracle baseline sample (0 disables it)")
     p.add_argument("--no-graph", dest="graph", action="store_false",
@@ -83,6 +87,17 @@ def algorithmic_bytes(cfg):
     select = q + index + tables
     attn = q + kv + n_sel * cfg.n_view * 4 + out
     return select, attn
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_oracle_baseline(w, seconds):
@@ -331,7 +346,8 @@ def recall_bench(args, cfg, seed):
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         n, el, cores = recall_baseline(w, args.cpu_seconds)
-        cpu = {"value": round(n / el, 5), "unit": "recalls/s", "cores": cores, "kind": "oracle",
+        cpu = {"value": round(n / el, 5), "unit": "recalls/s", "cores": cores, "cpu_model": cpu_model(),
+               "kind": "oracle",
                "sample": f"{n} full recall points of the same workload (fp64 Eq. 10 over every layer and "
                          f"query token, selection, working-set update; index built beforehand), {el:.1f}s"}
     res = {
@@ -395,14 +411,23 @@ def main():
     w = W.generate(cfg, seed, n_query_sets=args.query_sets)
     print(f"[bench] generated in {time.perf_counter() - t:.1f}s; uploading", file=sys.stderr, flush=True)
     dev = torch.device("cuda", 0)
-    layers = [LayerState(cfg, w.k_pool[l], w.v_pool[l], w.block_to_page, dev) for l in range(cfg.n_layers)]
+    # Infinity Cache defeat: a workload whose pools and index fit in or near the
+    # 256 MB cache is replicated, and step i runs on replica i mod R
+    footprint = cfg.n_layers * (2 * cfg.n_blocks * cfg.n_kv_heads * cfg.block_tokens * cfg.head_dim *
+                                cfg.elem_bytes + cfg.n_blocks * cfg.n_kv_heads * cfg.head_dim * 4)
+    n_rep = args.replicas if args.replicas is not None else \
+        (1 if footprint >= (2 << 30) else min(64, -(-(2 << 30) // footprint)))
+    reps = [[LayerState(cfg, w.k_pool[l], w.v_pool[l], w.block_to_page, dev) for l in range(cfg.n_layers)]
+            for _ in range(n_rep)]
+    layers = reps[0]
     qdev = torch.from_numpy(w.q).to(dev)  # [sets][L][n_q][Hq][d]
     torch.cuda.synchronize()
 
     # Mean-K index build (off the per-step path), timed separately
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for st in layers:
-        st.build_index()
+    for rep in reps:
+        for st in rep:
+            st.build_index()
     e0.record()
     for st in layers:
         st.build_index()
@@ -415,17 +440,29 @@ def main():
     stream = torch.cuda.current_stream()
     n_sets = qdev.shape[0]
 
-    def step(i, ev=None):
+    def step(i, rotate=True):
         qs = qdev[i % n_sets]
-        for l, st in enumerate(layers):
+        for l, st in enumerate(reps[i % n_rep] if rotate else layers):
             st.select(qs[l:l + 1], with_scores=False)
-            if ev is not None:
-                ev[0].record(stream)
             st.attend(qs[l])
-            if ev is not None:
-                ev[1].record(stream)
 
-    for i in range(args.warmup):
+    def graph_rate(n_graph, rotate, steps):
+        """ms per step replaying n_graph captured steps (one graph replay runs them all)."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n_graph):
+                step(i, rotate=rotate)
+        g.replay()
+        torch.cuda.synchronize()
+        reps_ = max(1, steps // n_graph)
+        print(f"[bench] timing {reps_ * n_graph} steps by graph replay", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        for _ in range(reps_):
+            g.replay()
+        torch.cuda.synchronize()
+        return g, reps_ * n_graph, (time.perf_counter() - t0) * 1000.0 / (reps_ * n_graph)
+
+    for i in range(max(args.warmup, n_rep)):
         step(i)
     torch.cuda.synchronize()
 
@@ -436,7 +473,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        for l, st in enumerate(layers):
+        for l, st in enumerate(reps[i % n_rep]):
             qs = qdev[i % n_sets]
             st.select(qs[l:l + 1], with_scores=False)
             a, b = evs[i * cfg.n_layers + l]
@@ -449,24 +486,24 @@ def main():
     n_steps, ms_per_step = args.steps, eager_ms
     graph = None
     if args.graph:
-        # the same steps, one per query set, captured once and replayed: every
-        # replay runs the whole selection and attention of each step again
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            for i in range(n_sets):
-                step(i)
-        graph.replay()
-        torch.cuda.synchronize()
-        reps = max(1, args.steps // n_sets)
-        print(f"[bench] timing {reps * n_sets} steps by graph replay", file=sys.stderr, flush=True)
-        torch.cuda.synchronize()
+        # the same steps (every query set on every replica) captured once and
+        # replayed: every replay runs the whole selection and attention again
+        graph, n_steps, ms_per_step = graph_rate(int(np.lcm(n_sets, n_rep)), True, args.steps)
+    cache = None
+    if n_rep > 1:
+        # the same steps on replica 0 only: the "hot" rate, with the pools and
+        # index (partly) resident in the Infinity Cache
         t0 = time.perf_counter()
-        for _ in range(reps):
-            graph.replay()
+        for i in range(args.steps):
+            step(i, rotate=False)
         torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        n_steps = reps * n_sets
-        ms_per_step = (t1 - t0) * 1000.0 / n_steps
+        hot_eager = (time.perf_counter() - t0) * 1000.0 / args.steps
+        hot = graph_rate(n_sets, False, args.steps)[2] if args.graph else hot_eager
+        cache = {"replicas": n_rep, "bytes_rotated_over": n_rep * footprint,
+                 "rotated_ms_per_step": round(ms_per_step, 5), "hot_ms_per_step": round(hot, 5),
+                 "hot_eager_ms_per_step": round(hot_eager, 5)}
+    else:
+        cache = {"replicas": 1, "bytes_rotated_over": footprint}
 
     sel_bytes, attn_bytes = algorithmic_bytes(cfg)
     step_bytes = cfg.n_layers * (sel_bytes + attn_bytes)
@@ -561,7 +598,8 @@ def main():
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         n, el, cores = cpu_oracle_baseline(w, args.cpu_seconds)
-        cpu = {"value": round(n / el, 4), "unit": "steps/s", "cores": cores, "kind": "oracle",
+        cpu = {"value": round(n / el, 4), "unit": "steps/s", "cores": cores, "cpu_model": cpu_model(),
+               "gpu_over_cpu": round((1000.0 / ms_per_step) / (n / el), 1), "kind": "oracle",
                "sample": f"{n} full decode steps of the same workload (fp64 relevance, selection and "
                          f"attention for every layer; index built beforehand), {el:.1f}s"}
 
@@ -592,6 +630,7 @@ def main():
         "step_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "index_build_GBps": round(build_bytes / (build_ms * 1e-3) / 1e9, 1),
         "timing_distribution": dist,
+        "infinity_cache": cache,
         "position_handling": position,
         "attainable_copy_GBps": copy_ref,
         "roofline": roofline,

@@ -285,7 +285,7 @@ size_t kvmem_select_workspace_bytes(const kvmem_geom *geom, int32_t n_layers, in
  *   q              dev  float [n_layers][n_q][Hq][d]
  *   index          dev  float, n_layers consecutive layers in the tiled
  *                       layout, each kvmem_index_bytes(geom, M) bytes
- *   n_blocks            M; requires n_sink + n_recent < M and |C| <= 65536
+ *   n_blocks            M; requires n_sink + n_recent < M and |C| <= 2^20
  *   model_ctx_tokens, gpu_kv_tokens   B_model and B_gpu of Eq. 5
  *   mode                kvmem_reduce
  *   scale               logit scale; <= 0 selects 1/sqrt(d)

@@ -962,9 +962,22 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int64_t stride = (int64_t)rows_total * (D + kPartStride);
     const float *pr = part + ((int64_t)g * n_splits * rows_total + r) * (D + kPartStride);
+    const int sl = tid / LPS, dq = tid % LPS;
 
-    float mx = -INFINITY;
-    for (int s = tid; s < n_splits; s += kCombineThreads) mx = fmaxf(mx, pr[s * stride + D]);
+    // one round trip for what most launches need: the thread's first PRE
+    // partial-row slices and (m, l) of split tid; later ones are read as used
+    constexpr int PRE = 8;
+    float4 held[PRE];
+#pragma unroll
+    for (int k = 0; k < PRE; ++k) {
+        const int s = sl + k * SPI;
+        held[k] = s < n_splits ? *reinterpret_cast<const float4 *>(pr + s * stride + dq * 4)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    const float m0 = tid < n_splits ? pr[tid * stride + D] : -INFINITY;
+    const float l0 = tid < n_splits ? pr[tid * stride + D + 1] : 0.f;
+    float mx = m0;
+    for (int s = tid + kCombineThreads; s < n_splits; s += kCombineThreads) mx = fmaxf(mx, pr[s * stride + D]);
     mx = wave_max(mx);
     if (lane == 0) sm_red[wave] = mx;
     __syncthreads();
@@ -974,10 +987,10 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     __syncthreads();
     float l = 0.f;
     for (int s = tid; s < n_splits; s += kCombineThreads) {
-        const float ms = pr[s * stride + D];
+        const float ms = s == tid ? m0 : pr[s * stride + D];
         const float f = ms == -INFINITY ? 0.f : exp2f(ms - mx);
         sm_w[s] = f;
-        l += pr[s * stride + D + 1] * f;
+        l += (s == tid ? l0 : pr[s * stride + D + 1]) * f;
     }
 #pragma unroll
     for (int o = kWave / 2; o >= 1; o >>= 1) l += shfl_xor_f(l, o);
@@ -987,10 +1000,17 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
 #pragma unroll
     for (int w = 0; w < kCombineThreads / kWave; ++w) l += sm_red[w];
 
-    const int sl = tid / LPS, dq = tid % LPS;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < PRE; ++k) {
+        const int s = sl + k * SPI;
+        if (s < n_splits) {
+            const float f = sm_w[s];
+            acc.x += held[k].x * f; acc.y += held[k].y * f; acc.z += held[k].z * f; acc.w += held[k].w * f;
+        }
+    }
 #pragma unroll 8
-    for (int s = sl; s < n_splits; s += SPI) {
+    for (int s = sl + PRE * SPI; s < n_splits; s += SPI) {
         const float4 v = *reinterpret_cast<const float4 *>(pr + s * stride + dq * 4);
         const float f = sm_w[s];
         acc.x += v.x * f; acc.y += v.y * f; acc.z += v.z * f; acc.w += v.w * f;

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
         const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
                                        (int64_t)(D / 4) * (kIndexTile * 4) + lane * 4;
 #pragma unroll
-        for (int j4 = 0; j4 < D / 4; ++j4) {  // every load of the tile in flight at once
+        for (int j4 = 0; j4 < D / 4; ++j4) {  // unrolled: the compiler keeps several loads in flight
             const float4 x = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
 #pragma unroll
             for (int r = 0; r < RH; ++r) {

@@ -83,12 +83,14 @@ __device__ void find_pivot(const uint32_t *__restrict__ gh, uint32_t k, uint32_t
     __syncthreads();
 }
 
-// Loads candidates 4t..4t+3 of chunk `chunk` (keys; 0 past n_cand).  Score
-// rows are padded to a multiple of 64 floats, so a float4 slot that starts
-// below n_cand is in bounds.
+// Loads candidates 4t..4t+3 of chunk `chunk` (keys; 0 past n_cand >= 1).
+// Score rows are padded to a multiple of 64 floats, so a float4 slot that
+// starts below n_cand is in bounds.
 __device__ inline void load_chunk_keys(const float *R, int chunk, int n_cand, uint32_t (&k)[4], int &c0) {
     c0 = chunk * kSelChunk + 4 * threadIdx.x;
-    const float4 x = c0 < n_cand ? *reinterpret_cast<const float4 *>(R + c0) : make_float4(0.f, 0.f, 0.f, 0.f);
+    // clamped rather than skipped: a load under a per-lane condition becomes a
+    // branch of its own, and the compiler then waits for each such load alone
+    const float4 x = *reinterpret_cast<const float4 *>(R + min(c0, (n_cand - 1) & ~3));
     const float v[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) k[e] = c0 + e < n_cand ? __float_as_uint(v[e]) + 1u : 0u;
@@ -114,15 +116,16 @@ __global__ __launch_bounds__(kChunkThreads) void sel_refine_kernel(
     const int chunk = blockIdx.x, sel = blockIdx.y;
     const SelHist h(hist, sel, gridDim.y);
     for (int i = threadIdx.x; i < kSelBins2; i += kChunkThreads) lh[i] = 0u;
+    // the chunk's keys do not depend on the pivot: read them with the histogram
+    uint32_t k[4];
+    int c0;
+    load_chunk_keys(r32 + (int64_t)sel * r_stride, chunk, n_cand, k, c0);
     uint32_t pivot, above_all;
     find_pivot<kChunkThreads, kSelBins>(h.h1, (uint32_t)k_eff, scratch, s_out, &pivot, &above_all);
     if (chunk == 0 && threadIdx.x == 0) {
         ctrl[sel * 8 + kCtrlPivot] = pivot;
         ctrl[sel * 8 + kCtrlRank] = (uint32_t)k_eff - above_all;  // rank inside the pivot bin
     }
-    uint32_t k[4];
-    int c0;
-    load_chunk_keys(r32 + (int64_t)sel * r_stride, chunk, n_cand, k, c0);
     uint32_t n_above = 0u, n_in = 0u;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -270,9 +273,30 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
     }
     if (k_eff <= 0) return;
     const SelHist h(hist, sel, gridDim.y);
+    const uint2 *row = seg + (int64_t)sel * n_chunks * kSelChunk;
+    // Everything that does not depend on this kernel's decisions is read up
+    // front, in one round trip: the first U pivot-bin items of each thread
+    // (read before their count is known; the array holds n_chunks * kSelChunk
+    // items, those past the count are ignored), the chunk's keys and their
+    // pages, and the selections above the pivot bin in the chunks before it.
+    constexpr int U = 8;  // pivot-bin items per thread in flight
+    const uint32_t cap = (uint32_t)n_chunks * kSelChunk;
+    uint2 first[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t i = (uint32_t)(tid + u * NT);
+        first[u] = row[min(i, cap - 1u)];
+    }
+    uint32_t k[4];
+    int c0;
+    load_chunk_keys(r32 + (int64_t)sel * r_stride, chunk, n_cand, k, c0);
+    int32_t pg[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pg[e] = block_to_page[n_sink + min(c0 + e, n_cand - 1)];
+    uint32_t before = 0u;  // selections of the chunks before this one
+    for (int i = tid; i < chunk; i += NT) before += above_cnt[(int64_t)sel * n_chunks + i];
     const uint32_t k_in = ctrl[sel * 8 + kCtrlRank];  // rank inside the pivot bin
     const uint32_t n_b = min(*h.count, (uint32_t)n_cand);  // keys in the pivot bin (<= n_cand)
-    const uint2 *row = seg + (int64_t)sel * n_chunks * kSelChunk;
     // sub-pivot bin and the rank inside it (its barriers also publish `above`)
     uint32_t sub, above_sub;
     find_pivot<NT, kSelBins2>(h.h2, k_in, sh.scratch, sh.s_out, &sub, &above_sub);
@@ -281,7 +305,7 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
     // one pass over the pivot-bin keys: those above the sub-pivot bin are
     // selected (count the ones of earlier chunks), the sub-pivot ones go to
     // this wave's part of the LDS window (no atomics: ballot + popcount)
-    uint32_t before = 0u, wn = 0u;
+    uint32_t wn = 0u;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
     auto visit = [&](bool valid, uint2 it) {
         const uint32_t b2 = bin2(it.x);
@@ -293,14 +317,15 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
         wn += (uint32_t)__popcll(m);
     };
     {
-        constexpr int U = 8;  // loads in flight per thread
         const int n_iter = (int)((n_b + NT - 1) / NT);
-        for (int j0 = 0; j0 < n_iter; j0 += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) visit((uint32_t)(tid + u * NT) < n_b, first[u]);
+        for (int j0 = U; j0 < n_iter; j0 += U) {
             uint2 it[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t i = (uint32_t)(tid + (j0 + u) * NT);
-                it[u] = i < n_b ? row[i] : make_uint2(0u, 0u);
+                it[u] = row[min(i, n_b - 1u)];  // n_b >= 1 here
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) visit((uint32_t)(tid + (j0 + u) * NT) < n_b, it[u]);
@@ -395,13 +420,9 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
     }
     const uint32_t thr = sh.s_thr, cut = sh.s_cut;
     // output offset of this chunk: every selection in the chunks before it
-    for (int i = tid; i < chunk; i += NT) before += above_cnt[(int64_t)sel * n_chunks + i];
     uint32_t base;
     block_exclusive_scan<NT>(before, sh.scratch, &base);
     // emit this chunk's selected candidates in order
-    uint32_t k[4];
-    int c0;
-    load_chunk_keys(r32 + (int64_t)sel * r_stride, chunk, n_cand, k, c0);
     bool take[4];
     uint32_t n_take = 0u;
 #pragma unroll
@@ -414,9 +435,8 @@ __global__ __launch_bounds__(kFinishThreads) void sel_finish_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         if (!take[e] || pos >= (uint32_t)k_eff) continue;  // pos < k_eff by construction
-        const int b = n_sink + c0 + e;
-        vb[n_sink + pos] = b;
-        vp[n_sink + pos] = block_to_page[b];
+        vb[n_sink + pos] = n_sink + c0 + e;
+        vp[n_sink + pos] = pg[e];
         ++pos;
     }
 }

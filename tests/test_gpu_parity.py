@@ -496,3 +496,43 @@ def test_all_equal_scores_beyond_2_16(k):
     torch.cuda.synchronize()
     vb = st.view_blocks.cpu().numpy()[0]
     assert vb.tolist() == list(range(k)) + list(range(m - 5, m))
+
+
+# ---- Exact ties at the threshold in rows beyond 2^17 candidates ------------
+def test_exact_ties_140k_candidates():
+    """140,000 candidates whose pages copy one of 100 source pages: ~1,400
+    exact ties per score (ranked by the radix select in LDS), the budget ends
+    inside them."""
+    m, n_src, extra = 140000 + 4, 100, 60000
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", m, 0, 4, 1, W.MEAN_ALL, extra, planted=0)
+    log(f"[case] exact ties, {cfg.n_candidates} candidates")
+    w = W.generate(cfg, 63, with_values=False)
+    kp = w.k_pool[0]
+    kp[:] = kp[np.random.default_rng(1).integers(0, n_src, cfg.n_blocks)]
+    index_ref = oracle.mean_k(kp, w.block_to_page)
+    rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 0, cfg.n_recent)
+    k_eff = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, 16, cfg.n_blocks, 0, cfg.n_recent)
+    vb_ref, _ = oracle.select(rel, 0, cfg.n_recent, k_eff, w.block_to_page)
+    st = LayerState(cfg, kp, None, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(st.view_blocks.cpu().numpy(), vb_ref)
+    np.testing.assert_array_equal(st.view_pages.cpu().numpy()[0], w.block_to_page[vb_ref[0]])
+
+
+@pytest.mark.parametrize("m,k", [(131072, 90000), (150000, 100000)])
+def test_all_equal_scores_150k(m, k):
+    """Up to 150,000 candidates with identical scores (the pivot bin far beyond
+    the LDS window): the selection is the k lowest ids."""
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", m + 5, 0, 5, 1, W.MEAN_ALL, k, planted=0)
+    log(f"[case] all scores equal, {cfg.n_candidates} candidates, k={k}")
+    w = W.generate(cfg, 64, with_values=False)
+    kp = np.broadcast_to(w.k_pool[0][:1], w.k_pool[0].shape).copy()
+    st = LayerState(cfg, kp, None, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    vb = st.view_blocks.cpu().numpy()[0]
+    assert vb.tolist() == list(range(k)) + list(range(m, m + 5))
+
