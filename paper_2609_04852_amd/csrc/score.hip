@@ -102,12 +102,17 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
 // logit is the fp32 rounding of the exact dot product (the vector kernel's
 // fp32 accumulation, and the fp32 matrix cores even more, lose a few ulps at
 // the logit magnitudes of clustered keys, which the selection's 1e-5 band
-// cannot afford).  One wave per (index tile, KV head) as above.  Per 16-block
-// group of the tile, S^T = index Q^T: lane l loads, for each 16-dim slice c,
-// the 4 dims 16c + 4kg .. of block l%16 (kg = l/16) as one float4 from the
-// tiled index and feeds them to 4 MFMAs whose contraction slot kg stands for
-// those dims; Q^T is the matching B operand, kept in registers.  Lane l
-// receives the logits of row l%16 for blocks kg, kg+4, kg+8, kg+12 of the group.
+// cannot afford).  One workgroup per (kMfma16Tiles index tiles, KV head):
+// wave w takes 16-block group w of each of the tiles, and issues the loads of
+// all of them before its first MFMA (a wave with a whole tile would load all
+// 64 blocks, then run 128 MFMAs in dependent chains with nothing else in
+// flight; with a group per tile, more waves fit a SIMD and the matrix unit
+// works on whichever wave's data has arrived).  For one group, S^T = index
+// Q^T: lane l loads, for each 16-dim slice c, the 4 dims 16c + 4kg .. of block
+// l%16 (kg = l/16) as one float4 from the tiled index and feeds them to 4
+// MFMAs whose contraction slot kg stands for those dims; Q^T is the matching B
+// operand, kept in registers.  Lane l receives the logits of row l%16 for
+// blocks kg, kg+4, kg+8, kg+12 of the group.
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
@@ -116,16 +121,28 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
     int n_tiles, int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
     double *__restrict__ tsum) {
-    constexpr int RH = 16, NW = kScoreThreads / kWave, NC = D / 16;
+    constexpr int RH = 16, NW = kScoreThreads / kWave, NC = D / 16, NT = kMfma16Tiles;
+    static_assert(NW * 16 == kIndexTile, "one 16-block group per wave");
     __shared__ float sm_m[NW][RH];
     __shared__ double sm_s[NW][RH];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r16 = lane % 16, kg = lane / 16;
-    const int g = blockIdx.y, l = blockIdx.z;
-    const int tile = tile_lo + blockIdx.x * NW + wave;
-    const bool tile_ok = blockIdx.x * NW + wave < n_tiles;
+    const int g = blockIdx.y, l = blockIdx.z, gb = wave;
     const int64_t qrow = ((int64_t)l * n_q + r16 / group) * n_q_heads + g * group + r16 % group;
+    const int64_t tiles_per_layer = index_tiles(n_blocks);
 
+    // the group's loads of every tile of the workgroup first (a tile past the
+    // candidates reads the last one again), then the query operand
+    float4 x[NT][NC];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int tile = tile_lo + min(blockIdx.x * NT + t, n_tiles - 1);
+        const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
+                                       (int64_t)(D / 4) * (kIndexTile * 4);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            x[t][c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4) + (16 * gb + r16) * 4);
+    }
     // B operand: q[row r16][16c + 4kg + e] (the scale is applied to the sum)
     float qv[NC][4];
 #pragma unroll
@@ -133,60 +150,45 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
         const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
         qv[c][0] = v.x; qv[c][1] = v.y; qv[c][2] = v.z; qv[c][3] = v.w;
     }
-    float s[4][4];  // [group][i]: row r16, block 16 * group + kg + 4i of the tile
-    if (tile_ok) {
-        const int64_t tiles_per_layer = index_tiles(n_blocks);
-        const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
-                                       (int64_t)(D / 4) * (kIndexTile * 4);
-        // all loads of the tile first, then four independent MFMA chains
-        float4 x[4][NC];
+    __builtin_amdgcn_sched_barrier(0);  // keep every load in flight together
+    float s[NT][4];  // tile t, row r16, block 16 * gb + kg + 4i
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int gb = 0; gb < 4; ++gb)
-                x[gb][c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4) +
-                                                               (16 * gb + r16) * 4);
-        __builtin_amdgcn_sched_barrier(0);  // keep every load of the tile in flight together
-        f64x4_t st[4];
-#pragma unroll
-        for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+    for (int t = 0; t < NT; ++t) {
+        f64x4_t st = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
+                st = __builtin_amdgcn_mfma_f64_16x16x4f64((double)x[t][c][e], (double)qv[c][e], st, 0, 0, 0);
 #pragma unroll
-                for (int gb = 0; gb < 4; ++gb)
-                    st[gb] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)x[gb][c][e], (double)qv[c][e], st[gb],
-                                                                  0, 0, 0);
-#pragma unroll
-        for (int gb = 0; gb < 4; ++gb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s[gb][i] = (float)(st[gb][i] * (double)scale);
+        for (int i = 0; i < 4; ++i) s[t][i] = (float)(st[i] * (double)scale);
     }
-    // logits (4 consecutive blocks per lane and group) and per-row stats
-    const int64_t b0 = (int64_t)tile * kIndexTile;
+    // logits (4 blocks per lane and tile, 4 apart) and per-row stats
+    auto valid = [&](int t, int i, int64_t &c) {
+        c = (int64_t)(tile_lo + blockIdx.x * NT + t) * kIndexTile + 16 * gb + kg + 4 * i - n_sink;
+        return blockIdx.x * NT + t < n_tiles && c >= 0 && c < n_cand;
+    };
     float mx = -INFINITY;
 #pragma unroll
-    for (int gb = 0; gb < 4; ++gb) {
-        const int64_t c0 = b0 + 16 * gb + kg - n_sink;  // candidate of i = 0
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const bool ok = tile_ok && c0 + 4 * i >= 0 && c0 + 4 * i < n_cand;
-            if (ok) logits[qrow * cand_stride + c0 + 4 * i] = s[gb][i];
-            mx = fmaxf(mx, ok ? s[gb][i] : -INFINITY);
+            int64_t c;
+            const bool ok = valid(t, i, c);
+            if (ok) logits[qrow * cand_stride + c] = s[t][i];
+            mx = fmaxf(mx, ok ? s[t][i] : -INFINITY);
         }
-    }
     mx = fmaxf(mx, shfl_xor_f(mx, 16));
     mx = fmaxf(mx, shfl_xor_f(mx, 32));
     double e = 0.0;
     if (mx != -INFINITY) {
 #pragma unroll
-        for (int gb = 0; gb < 4; ++gb) {
-            const int64_t c0 = b0 + 16 * gb + kg - n_sink;
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (tile_ok && c0 + 4 * i >= 0 && c0 + 4 * i < n_cand) e += (double)expf(s[gb][i] - mx);
-        }
+            for (int i = 0; i < 4; ++i) {
+                int64_t c;
+                if (valid(t, i, c)) e += (double)expf(s[t][i] - mx);
+            }
     }
     e += __shfl_xor(e, 16, kWave);
     e += __shfl_xor(e, 32, kWave);
