@@ -113,6 +113,9 @@ SHAPES = [
     (2, 8, 128, 64, "bf16", 260, 0, 2, 4, W.MAX_GROUP, 37),
     # fp32 K/V, d128, 64-token pages, 8 rows per KV head (two 4-row workgroups)
     (2, 16, 128, 64, "f32", 150, 0, 2, 1, W.MEAN_ALL, 20),
+    # the largest KV head count the library takes (64), no grouping
+    (64, 64, 64, 16, "bf16", 200, 1, 2, 1, W.MAX_GROUP, 30),
+    (64, 128, 128, 32, "bf16", 150, 0, 3, 2, W.MEAN_ALL, 25),
 ]
 
 
