@@ -1,6 +1,16 @@
 // Decode attention over the execution view through its page table (Sec. 4.4,
 // Sec. 5.3): split-K flash-decode plus an exact log-sum-exp merge.
 //
+// Kernels, by shape (launch_bt picks one; every one writes the same partials):
+//   attn_mfma16        bf16 K/V with 4 to 47 query rows per KV head, and FP8
+//                      below 48 rows: both products on the matrix cores
+//   attn_mfma_rows     48 or more rows (bf16, FP8): groups of 16-row waves
+//                      share each K/V tile through LDS
+//   attn_splitk_row16  fp32 K/V at d = 64 with a multiple of 4 rows (a token
+//                      row is one 16-lane DPP row), vector units
+//   attn_splitk        every other shape, vector units
+//   attn_combine       the exact merge of a (KV head, row)'s split partials
+//
 // attn_splitk: one workgroup per (split of the view, KV head, chunk of query
 // rows).  The rows of a KV head are the G * n_q (query token, query head) pairs
 // that read it (GQA), so every K/V byte fetched serves all of them.  A token's
