@@ -5,7 +5,7 @@
 // One workgroup per (64-block tile, KV head).  Each wave reduces 16 of the
 // tile's blocks: a page slice [Bt][d] is contiguous, so LPR = d*elem/16 lanes
 // read one token row with 16-byte loads and 64/LPR rows go per instruction;
-// four blocks are loaded per step to keep loads in flight.  Sums are kept in
+// the loads of 16 tokens of several blocks are issued together (see below).  Sums are kept in
 // fp64: adding Bt <= 64 bf16 values (8-bit significands) or fp32 values whose
 // magnitudes span less than 2^23 is exact there, so the result -- rounded once
 // to fp32 -- does not depend on the order of summation.  The finished means
@@ -23,15 +23,36 @@ namespace kvmem {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kBlocksPerStep = 4;
 
 // ROPE: the stored keys carry RoPE (rotate-half form) at positions
 // block_pos[b] + t (block_pos NULL: b * block_tokens + t); each token row is
 // turned back to position 0 before it enters the sum (Sec. 4.3: the index is
 // built from position-independent keys).  The lane holding dims [j, j+VEC)
 // of one half gets the matching dims of the other half from lane lp ^ LPR/2.
-// Angles are formed and reduced in fp64 (rope_cos_sin), cos/sin and the
-// rotation in fp32.
+// The angle of token t is the fp64 product a_t = (p0 + t) f_j (as in the
+// definition), turned into a rotation without a sin/cos per token: with
+// a_0 = p0 f_j (its cos/sin taken once per block and pair, the angle reduced
+// in fp64 by rope_cos_sin) and the cos/sin of t f_j from a per-workgroup LDS
+// table, a_t = a_0 + t f_j + eps, where eps = (a_t - a_0) - t f_j is the
+// rounding of the products (computed exactly enough in fp64: a_t - a_0 is
+// exact there).  The three rotations are composed in fp32, eps to first order
+// (cos eps = 1 - eps^2/2, and eps stays below an fp64 ulp of the angle: 2.4e-4
+// rad even at positions of 2^40).  That is sixteen to sixty-four times fewer
+// sin/cos than one per token, at about two fp32 ulps of the cos and sin.
+//
+// Every block_tokens is a multiple of 16, so a wave reads a block 16 tokens
+// at a time: NI = 16 / TG loads per lane, all issued before the first sum,
+// for BPS blocks at once (about 16 loads of 16 bytes in flight per lane).
+
+constexpr int kMaxBlockTokens = 64;
+
+// eps = (a_t - a_0) - t f with each product rounded on its own, as the angle
+// a_t = (p0 + t) f is defined (a fused multiply-add would skip a rounding)
+__device__ inline float rope_eps(int64_t p0, int t, double f) {
+#pragma clang fp contract(off)
+    const double at = (double)(p0 + t) * f, a0 = (double)p0 * f, tf = (double)t * f;
+    return (float)((at - a0) - tf);
+}
 
 template <typename T, int D, bool ROPE>
 __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
@@ -41,12 +62,19 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     constexpr int VEC = Vec16<T>::N;  // elements per lane per row
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
+    constexpr int NI = 16 / TG;       // instructions per 16 tokens
+    static_assert(NI * TG == 16, "16 tokens split over whole instructions");
     constexpr int PAD = D + 4;        // LDS row stride (floats): conflict-free column reads
     constexpr bool F8 = sizeof(T) == 1;
     // exact sums: fp32 for unrotated FP8 codes, fp64 otherwise
     using Acc = typename std::conditional<F8 && !ROPE, float, double>::type;
-    constexpr int BPS = F8 && ROPE ? 2 : kBlocksPerStep;  // 16 values per lane: fewer blocks in flight
+    // blocks per step: about 16 loads in flight per lane; the rotation's
+    // per-block cos/sin take registers, so fewer blocks with RoPE
+    constexpr int BPS0 = 16 / NI > 4 ? 4 : 16 / NI;
+    constexpr int BPS = !ROPE ? BPS0 : VEC >= 16 ? 1 : BPS0 > 1 ? BPS0 / 2 : 1;
+    constexpr int RB = ROPE ? BPS : 1, RV = ROPE ? VEC : 1;  // sizes of the per-block rotation
     __shared__ float tile_buf[kIndexTile * PAD];
+    __shared__ float2 rot_t[ROPE ? kMaxBlockTokens * (D / 2) : 1];  // (cos, sin) of t * f_j
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int tg = lane / LPR, lp = lane % LPR;
@@ -58,6 +86,15 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const int64_t b_hi = b_tile0 + kIndexTile < b_end ? b_tile0 + kIndexTile : b_end;
     const double inv = 1.0 / (double)block_tokens, ks = (double)k_scale;
     const int j0 = (lp % (LPR / 2)) * VEC;  // RoPE pair index of this lane's element 0
+    const bool upper = lp >= LPR / 2;       // the lane holds x_{j + d/2}
+    if constexpr (ROPE) {
+        for (int i = threadIdx.x; i < block_tokens * (D / 2); i += kWaves * kWave) {
+            float c, sn;
+            rope_cos_sin(i / (D / 2), fr.f[i % (D / 2)], &c, &sn);
+            rot_t[i] = make_float2(c, sn);
+        }
+        __syncthreads();
+    }
 
     // wave w reduces tile slots w, w+4, w+8, ... (BPS at a time)
     for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * BPS) {
@@ -65,50 +102,59 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         double mean[VEC];
         bool ok[BPS];
         const T *base[BPS];
-        int64_t p0[BPS];
+        float c0[RB][RV], s0v[RB][RV];  // cos, sin of a_0 = p0 * f_j for the lane's pairs
+        int64_t p0[RB];
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
             const bool in = b >= b_lo && b < b_hi;
             const int64_t page = in ? block_to_page[b] : -1;
             ok[k] = in && page >= 0 && page < n_pages;
+            // a block outside the range or without a valid page reads page 0
+            // (in bounds) and is written as NaN
             base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D + lp * VEC;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[k][e] = 0;
-            p0[k] = ROPE && block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
-        }
-        for (int t = tg; t < block_tokens; t += TG) {
-            float v[BPS][VEC];
-#pragma unroll
-            for (int k = 0; k < BPS; ++k) {
-                if (ok[k]) {
-                    Vec16<T>::load(base[k] + (int64_t)t * D, v[k]);
-                } else {
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) v[k][e] = 0.f;
-                }
-            }
             if constexpr (ROPE) {
-                const bool upper = lp >= LPR / 2;
+                p0[k] = block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
 #pragma unroll
-                for (int k = 0; k < BPS; ++k) {
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const float other = __shfl_xor(v[k][e], LPR / 2, kWave);
-                        // the angle (p0 + t) * f_j, formed as one fp64 product: the
-                        // sum of the start and offset angles would round differently
-                        // at large positions
-                        float c, sn;
-                        rope_cos_sin(p0[k] + t, fr.f[j0 + e], &c, &sn);
-                        // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
-                        v[k][e] = upper ? v[k][e] * c - other * sn : v[k][e] * c + other * sn;
-                    }
-                }
+                for (int e = 0; e < VEC; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
             }
+        }
+        for (int t0 = 0; t0 < block_tokens; t0 += 16) {
+            uint4 raw[BPS][NI];
 #pragma unroll
             for (int k = 0; k < BPS; ++k)
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) acc[k][e] += (Acc)v[k][e];
+                for (int i = 0; i < NI; ++i) raw[k][i] = load_stream16(base[k] + (int64_t)(t0 + tg + TG * i) * D);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int t = t0 + tg + TG * i;
+                float2 rt[RV];
+                if constexpr (ROPE) {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
+                }
+#pragma unroll
+                for (int k = 0; k < BPS; ++k) {
+                    float v[VEC];
+                    Vec16<T>::decode(raw[k][i], v);
+                    if constexpr (ROPE) {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            const float other = __shfl_xor(v[e], LPR / 2, kWave);
+                            const float eps = rope_eps(p0[k], t, fr.f[j0 + e]);
+                            const float cc = c0[k][e] * rt[e].x - s0v[k][e] * rt[e].y;
+                            const float ss = s0v[k][e] * rt[e].x + c0[k][e] * rt[e].y;
+                            const float c = cc - ss * eps, sn = ss + cc * eps;
+                            // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
+                            v[e] = upper ? v[e] * c - other * sn : v[e] * c + other * sn;
+                        }
+                    }
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[k][e] += (Acc)v[e];
+                }
+            }
         }
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {

@@ -31,18 +31,18 @@ struct Vec16;
 template <>
 struct Vec16<float> {
     static constexpr int N = 4;
-    __device__ static inline void load(const float *p, float (&out)[4]) {
-        const uint4 v = load_stream16(p);
+    __device__ static inline void decode(const uint4 &v, float (&out)[4]) {
         out[0] = __uint_as_float(v.x); out[1] = __uint_as_float(v.y);
         out[2] = __uint_as_float(v.z); out[3] = __uint_as_float(v.w);
     }
+    __device__ static inline void load(const float *p, float (&out)[4]) { decode(load_stream16(p), out); }
 };
 
 template <>
 struct Vec16<uint16_t> {
     static constexpr int N = 8;
-    __device__ static inline void load(const uint16_t *p, float (&out)[8]) {
-        const uint4 v = load_stream16(p);
+    __device__ static inline void load(const uint16_t *p, float (&out)[8]) { decode(load_stream16(p), out); }
+    __device__ static inline void decode(const uint4 &v, float (&out)[8]) {
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -59,8 +59,8 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 template <>
 struct Vec16<uint8_t> {
     static constexpr int N = 16;
-    __device__ static inline void load(const uint8_t *p, float (&out)[16]) {
-        const uint4 v = load_stream16(p);
+    __device__ static inline void load(const uint8_t *p, float (&out)[16]) { decode(load_stream16(p), out); }
+    __device__ static inline void decode(const uint4 &v, float (&out)[16]) {
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
