@@ -39,12 +39,14 @@ constexpr int kWaves = 4;
 // (cos eps = 1 - eps^2/2, and eps stays below an fp64 ulp of the angle: 2.4e-4
 // rad even at positions of 2^40).  That is sixteen to sixty-four times fewer
 // sin/cos than one per token, at about two fp32 ulps of the cos and sin.
+// Below kEpsMinPos (2^26) eps is under 1.5e-8 rad and is left out.
 //
 // Every block_tokens is a multiple of 16, so a wave reads a block 16 tokens
 // at a time: NI = 16 / TG loads per lane, all issued before the first sum,
 // for BPS blocks at once (about 16 loads of 16 bytes in flight per lane).
 
 constexpr int kMaxBlockTokens = 64;
+constexpr int64_t kEpsMinPos = int64_t(1) << 26;
 
 // eps = (a_t - a_0) - t f with each product rounded on its own, as the angle
 // a_t = (p0 + t) f is defined (a fused multiply-add would skip a rounding)
@@ -104,6 +106,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         const T *base[BPS];
         float c0[RB][RV], s0v[RB][RV];  // cos, sin of a_0 = p0 * f_j for the lane's pairs
         int64_t p0[RB];
+        bool far[RB];  // positions reach kEpsMinPos: correct for the rounding of the products
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
@@ -117,45 +120,63 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
             for (int e = 0; e < VEC; ++e) acc[k][e] = 0;
             if constexpr (ROPE) {
                 p0[k] = block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
+                far[k] = !(p0[k] > -kEpsMinPos && p0[k] + block_tokens <= kEpsMinPos);
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
             }
         }
-        for (int t0 = 0; t0 < block_tokens; t0 += 16) {
-            uint4 raw[BPS][NI];
+        // the token loop, compiled with and without the rounding correction
+        auto sum_tokens = [&](auto with_eps) {
+            for (int t0 = 0; t0 < block_tokens; t0 += 16) {
+                uint4 raw[BPS][NI];
 #pragma unroll
-            for (int k = 0; k < BPS; ++k)
+                for (int k = 0; k < BPS; ++k)
 #pragma unroll
-                for (int i = 0; i < NI; ++i) raw[k][i] = load_stream16(base[k] + (int64_t)(t0 + tg + TG * i) * D);
+                    for (int i = 0; i < NI; ++i)
+                        raw[k][i] = load_stream16(base[k] + (int64_t)(t0 + tg + TG * i) * D);
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const int t = t0 + tg + TG * i;
-                float2 rt[RV];
-                if constexpr (ROPE) {
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
-                }
-#pragma unroll
-                for (int k = 0; k < BPS; ++k) {
-                    float v[VEC];
-                    Vec16<T>::decode(raw[k][i], v);
+                for (int i = 0; i < NI; ++i) {
+                    const int t = t0 + tg + TG * i;
+                    float2 rt[RV];
                     if constexpr (ROPE) {
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) {
-                            const float other = __shfl_xor(v[e], LPR / 2, kWave);
-                            const float eps = rope_eps(p0[k], t, fr.f[j0 + e]);
-                            const float cc = c0[k][e] * rt[e].x - s0v[k][e] * rt[e].y;
-                            const float ss = s0v[k][e] * rt[e].x + c0[k][e] * rt[e].y;
-                            const float c = cc - ss * eps, sn = ss + cc * eps;
-                            // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
-                            v[e] = upper ? v[e] * c - other * sn : v[e] * c + other * sn;
-                        }
+                        for (int e = 0; e < VEC; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
                     }
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[k][e] += (Acc)v[e];
+                    for (int k = 0; k < BPS; ++k) {
+                        float v[VEC];
+                        Vec16<T>::decode(raw[k][i], v);
+                        if constexpr (ROPE) {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                const float other = __shfl_xor(v[e], LPR / 2, kWave);
+                                float c = c0[k][e] * rt[e].x - s0v[k][e] * rt[e].y;
+                                float sn = s0v[k][e] * rt[e].x + c0[k][e] * rt[e].y;
+                                if constexpr (decltype(with_eps)::value) {
+                                    const float eps = rope_eps(p0[k], t, fr.f[j0 + e]);
+                                    const float cc = c;
+                                    c = cc - sn * eps;
+                                    sn = sn + cc * eps;
+                                }
+                                // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
+                                v[e] = upper ? v[e] * c - other * sn : v[e] * c + other * sn;
+                            }
+                        }
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[k][e] += (Acc)v[e];
+                    }
                 }
             }
+        };
+        bool any_far = false;
+        if constexpr (ROPE) {
+#pragma unroll
+            for (int k = 0; k < BPS; ++k) any_far |= far[k];
         }
+        if (any_far)  // wave-uniform
+            sum_tokens(std::true_type{});
+        else
+            sum_tokens(std::false_type{});
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
 #pragma unroll
