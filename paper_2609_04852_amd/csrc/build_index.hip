@@ -27,8 +27,9 @@ constexpr int kWaves = 4;
 // ROPE: the stored keys carry RoPE (rotate-half form) at positions
 // block_pos[b] + t (block_pos NULL: b * block_tokens + t); each token row is
 // turned back to position 0 before it enters the sum (Sec. 4.3: the index is
-// built from position-independent keys).  The lane holding dims [j, j+VEC)
-// of one half gets the matching dims of the other half from lane lp ^ LPR/2.
+// built from position-independent keys).  A lane then reads its row as two
+// 8-byte pieces, the VEC/2 dims [j0, j0 + VEC/2) and the matching dims of the
+// other half, so that it holds both members of its pairs.
 // The angle of token t is the fp64 product a_t = (p0 + t) f_j (as in the
 // definition), turned into a rotation without a sin/cos per token: with
 // a_0 = p0 f_j (its cos/sin taken once per block and pair, the angle reduced
@@ -73,8 +74,8 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     // blocks per step: about 16 loads in flight per lane; the rotation's
     // per-block cos/sin take registers, so fewer blocks with RoPE
     constexpr int BPS0 = 16 / NI > 4 ? 4 : 16 / NI;
-    constexpr int BPS = !ROPE ? BPS0 : VEC >= 16 ? 1 : BPS0 > 1 ? BPS0 / 2 : 1;
-    constexpr int RB = ROPE ? BPS : 1, RV = ROPE ? VEC : 1;  // sizes of the per-block rotation
+    constexpr int BPS = !ROPE || BPS0 == 1 ? BPS0 : BPS0 / 2;
+    constexpr int RB = ROPE ? BPS : 1, RV = ROPE ? VEC / 2 : 1;  // sizes of the per-block rotation
     __shared__ float tile_buf[kIndexTile * PAD];
     __shared__ float2 rot_t[ROPE ? kMaxBlockTokens * (D / 2) : 1];  // (cos, sin) of t * f_j
 
@@ -87,8 +88,8 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const int64_t b_end = (int64_t)first_block + n_blocks;
     const int64_t b_hi = b_tile0 + kIndexTile < b_end ? b_tile0 + kIndexTile : b_end;
     const double inv = 1.0 / (double)block_tokens, ks = (double)k_scale;
-    const int j0 = (lp % (LPR / 2)) * VEC;  // RoPE pair index of this lane's element 0
-    const bool upper = lp >= LPR / 2;       // the lane holds x_{j + d/2}
+    constexpr int HV = VEC / 2;           // RoPE: pairs per lane
+    const int j0 = lp * HV;               // RoPE: the lane's first pair
     if constexpr (ROPE) {
         for (int i = threadIdx.x; i < block_tokens * (D / 2); i += kWaves * kWave) {
             float c, sn;
@@ -115,14 +116,15 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
             ok[k] = in && page >= 0 && page < n_pages;
             // a block outside the range or without a valid page reads page 0
             // (in bounds) and is written as NaN
-            base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D + lp * VEC;
+            base[k] = k_pool + ((ok[k] ? page : 0) * n_kv_heads + g) * (int64_t)block_tokens * D +
+                      (ROPE ? j0 : lp * VEC);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[k][e] = 0;
             if constexpr (ROPE) {
                 p0[k] = block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
                 far[k] = !(p0[k] > -kEpsMinPos && p0[k] + block_tokens <= kEpsMinPos);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
+                for (int e = 0; e < HV; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
             }
         }
         // the token loop, compiled with and without the rounding correction
@@ -132,15 +134,22 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
                 for (int k = 0; k < BPS; ++k)
 #pragma unroll
-                    for (int i = 0; i < NI; ++i)
-                        raw[k][i] = load_stream16(base[k] + (int64_t)(t0 + tg + TG * i) * D);
+                    for (int i = 0; i < NI; ++i) {
+                        const T *row = base[k] + (int64_t)(t0 + tg + TG * i) * D;
+                        if constexpr (ROPE) {
+                            const uint2 lo = load_stream8(row), hi = load_stream8(row + D / 2);
+                            raw[k][i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                        } else {
+                            raw[k][i] = load_stream16(row);
+                        }
+                    }
 #pragma unroll
                 for (int i = 0; i < NI; ++i) {
                     const int t = t0 + tg + TG * i;
                     float2 rt[RV];
                     if constexpr (ROPE) {
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
+                        for (int e = 0; e < HV; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
                     }
 #pragma unroll
                     for (int k = 0; k < BPS; ++k) {
@@ -148,8 +157,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                         Vec16<T>::decode(raw[k][i], v);
                         if constexpr (ROPE) {
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) {
-                                const float other = __shfl_xor(v[e], LPR / 2, kWave);
+                            for (int e = 0; e < HV; ++e) {  // pair j0 + e: v[e] and v[HV + e]
                                 float c = c0[k][e] * rt[e].x - s0v[k][e] * rt[e].y;
                                 float sn = s0v[k][e] * rt[e].x + c0[k][e] * rt[e].y;
                                 if constexpr (decltype(with_eps)::value) {
@@ -158,8 +166,10 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                                     c = cc - sn * eps;
                                     sn = sn + cc * eps;
                                 }
-                                // turn by -angle: lower x_j c + x_{j+h} s, upper -x_j s + x_{j+h} c
-                                v[e] = upper ? v[e] * c - other * sn : v[e] * c + other * sn;
+                                // turn by -angle: x_j c + x_{j+h} s, -x_j s + x_{j+h} c
+                                const float lo = v[e], hi = v[HV + e];
+                                v[e] = lo * c + hi * sn;
+                                v[HV + e] = hi * c - lo * sn;
                             }
                         }
 #pragma unroll
@@ -186,13 +196,19 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
             for (int e = 0; e < VEC; ++e) mean[e] = (double)acc[k][e] * ks * inv;
             if (tg == 0) {
-                float *dst = tile_buf + (s0 + k * kWaves) * PAD + lp * VEC;
+                float *dst = tile_buf + (s0 + k * kWaves) * PAD;
+                if constexpr (ROPE) {  // dims j0 + e and D/2 + j0 + e
 #pragma unroll
-                for (int e = 0; e < VEC; e += 4)
-                    *reinterpret_cast<float4 *>(dst + e) = ok[k]
-                        ? make_float4((float)mean[e], (float)mean[e + 1], (float)mean[e + 2], (float)mean[e + 3])
-                        : make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
-                                      __builtin_nanf(""));
+                    for (int e = 0; e < VEC; ++e)
+                        dst[e < HV ? j0 + e : D / 2 + j0 + e - HV] = ok[k] ? (float)mean[e] : __builtin_nanf("");
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VEC; e += 4)
+                        *reinterpret_cast<float4 *>(dst + lp * VEC + e) = ok[k]
+                            ? make_float4((float)mean[e], (float)mean[e + 1], (float)mean[e + 2], (float)mean[e + 3])
+                            : make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
+                                          __builtin_nanf(""));
+                }
             }
         }
     }

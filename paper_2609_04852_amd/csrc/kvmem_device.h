@@ -23,6 +23,14 @@ __device__ inline uint4 load_stream16(const T *p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// The same for 8 bytes.
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ inline uint2 load_stream8(const T *p) {
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t *>(p));
+    return make_uint2(v.x, v.y);
+}
+
 // One 16-byte load of K/V elements widened to fp32.  bf16 values are stored as
 // raw 16-bit patterns; widening is exact.
 template <typename T>
