@@ -222,6 +222,24 @@ __device__ inline double wave_sum_d(double v) {
     return v;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave on the DPP lane paths
+// (no LDS round trip): a Kogge-Stone scan inside each 16-lane row by
+// row_shr 1, 2, 4, 8, then row_bcast:15 adds row 0's total to row 1 and row
+// 2's to row 3, and row_bcast:31 adds the total of rows 0-1 to rows 2-3.
+// Lanes without a source (and rows the mask leaves out) add 0.
+constexpr int kDppRowShr = 0x110;      // row_shr:n is kDppRowShr + n
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+__device__ inline uint32_t wave_inclusive_scan(uint32_t x) {
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 1, 0xf, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 2, 0xf, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 4, 0xf, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 8, 0xf, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowBcast15, 0xa, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowBcast31, 0xc, 0xf, false);
+    return x;
+}
+
 // Exclusive prefix sum of one uint32 per thread across a workgroup of
 // NT threads (multiple of 64).  `scratch` needs NT/64 + 1 entries.  Returns
 // the exclusive prefix; *total receives the workgroup sum.
@@ -229,22 +247,12 @@ template <int NT>
 __device__ inline uint32_t block_exclusive_scan(uint32_t x, uint32_t *scratch, uint32_t *total) {
     constexpr int NW = NT / kWave;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    uint32_t incl = x;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        uint32_t y = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += y;
-    }
+    const uint32_t incl = wave_inclusive_scan(x);
     if (lane == kWave - 1) scratch[wave] = incl;
     __syncthreads();
     if (wave == 0) {
-        uint32_t t = lane < NW ? scratch[lane] : 0u;
-        uint32_t ti = t;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            uint32_t y = __shfl_up(ti, o, kWave);
-            if (lane >= o) ti += y;
-        }
+        const uint32_t t = lane < NW ? scratch[lane] : 0u;
+        const uint32_t ti = wave_inclusive_scan(t);
         if (lane < NW) scratch[lane] = ti - t;  // exclusive wave offsets
         if (lane == NW - 1) scratch[NW] = ti;
     }
