@@ -1002,8 +1002,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
         sm_w[s] = f;
         l += (s == tid ? l0 : pr[s * stride + D + 1]) * f;
     }
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) l += shfl_xor_f(l, o);
+    l = wave_sum_f(l);
     if (lane == 0) sm_red[wave] = l;
     __syncthreads();
     l = 0.f;

@@ -210,16 +210,59 @@ __device__ inline float team_sum(float v) {
     return v;
 }
 
+// Reductions over a whole wave on the DPP lane paths (no LDS round trip):
+// inside each 16-lane row by quad_perm xor 1, xor 2 and row_ror 4, 8 (every
+// lane then holds its row's result), then row_bcast:15 takes rows 0 and 2
+// into rows 1 and 3 and row_bcast:31 takes row 1 into rows 2 and 3 (rows the
+// mask leaves out read the identity), and lane 63's result goes to every lane.
+// Every lane of the wave must be active.
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ inline float dpp_or(float x, float identity) {
+    return __int_as_float(
+        __builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(x), CTRL, ROW_MASK, 0xF, false));
+}
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ inline double dpp_d0(double x) {  // identity 0.0: all bits zero
+    const uint64_t b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROW_MASK, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROW_MASK, 0xF, false);
+    return __longlong_as_double((int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
 __device__ inline float wave_max(float v) {
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) v = fmaxf(v, shfl_xor_f(v, o));
-    return v;
+    const float id = -INFINITY;
+    v = fmaxf(v, dpp_or<kDppQuadXor1>(v, id));
+    v = fmaxf(v, dpp_or<kDppQuadXor2>(v, id));
+    v = fmaxf(v, dpp_or<dpp_row_ror(4)>(v, id));
+    v = fmaxf(v, dpp_or<dpp_row_ror(8)>(v, id));
+    v = fmaxf(v, dpp_or<kDppRowBcast15, 0xA>(v, id));
+    v = fmaxf(v, dpp_or<kDppRowBcast31, 0xC>(v, id));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
+}
+
+__device__ inline float wave_sum_f(float v) {
+    v += dpp_or<kDppQuadXor1>(v, 0.f);
+    v += dpp_or<kDppQuadXor2>(v, 0.f);
+    v += dpp_or<dpp_row_ror(4)>(v, 0.f);
+    v += dpp_or<dpp_row_ror(8)>(v, 0.f);
+    v += dpp_or<kDppRowBcast15, 0xA>(v, 0.f);
+    v += dpp_or<kDppRowBcast31, 0xC>(v, 0.f);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
 }
 
 __device__ inline double wave_sum_d(double v) {
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) v += shfl_xor_d(v, o);
-    return v;
+    v += dpp_d0<kDppQuadXor1>(v);
+    v += dpp_d0<kDppQuadXor2>(v);
+    v += dpp_d0<dpp_row_ror(4)>(v);
+    v += dpp_d0<dpp_row_ror(8)>(v);
+    v += dpp_d0<kDppRowBcast15, 0xA>(v);
+    v += dpp_d0<kDppRowBcast31, 0xC>(v);
+    const uint64_t b = __double_as_longlong(v);
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, kWave - 1);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), kWave - 1);
+    return __longlong_as_double((int64_t)(((uint64_t)hi << 32) | lo));
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave on the DPP lane paths
@@ -228,8 +271,6 @@ __device__ inline double wave_sum_d(double v) {
 // 2's to row 3, and row_bcast:31 adds the total of rows 0-1 to rows 2-3.
 // Lanes without a source (and rows the mask leaves out) add 0.
 constexpr int kDppRowShr = 0x110;      // row_shr:n is kDppRowShr + n
-constexpr int kDppRowBcast15 = 0x142;
-constexpr int kDppRowBcast31 = 0x143;
 __device__ inline uint32_t wave_inclusive_scan(uint32_t x) {
     x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 1, 0xf, 0xf, false);
     x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppRowShr + 2, 0xf, 0xf, false);
