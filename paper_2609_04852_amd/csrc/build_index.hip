@@ -47,6 +47,46 @@ constexpr int kWaves = 4;
 // for BPS blocks at once (about 16 loads of 16 bytes in flight per lane).
 
 constexpr int kMaxBlockTokens = 64;
+
+// Sum over the lanes of the wave that share lane % L (L = 4 .. 32, a power of
+// two): inside each 16-lane row by row_ror L, 2L, .. 8 (DPP), then across
+// rows by the permlane swaps (xor 16, xor 32), every lane ending with its
+// class's sum.  All register moves, no LDS.  Every lane must be active.
+template <int CTRL>
+__device__ inline uint32_t dpp_u(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+template <int L, typename V>
+__device__ inline V sum_lanes_mod(V v) {
+    static_assert(L >= 4 && L <= 32 && (L & (L - 1)) == 0, "lane classes of 4 .. 32");
+    auto move = [](V x, auto op) {  // apply op to each 32-bit half of x
+        if constexpr (sizeof(V) == 8) {
+            const uint64_t b = __double_as_longlong(x);
+            const uint64_t lo = op((uint32_t)b), hi = op((uint32_t)(b >> 32));
+            return __longlong_as_double((int64_t)((hi << 32) | lo));
+        } else {
+            return __uint_as_float(op(__float_as_uint(x)));
+        }
+    };
+    if constexpr (L <= 4) v += move(v, [](uint32_t x) { return dpp_u<dpp_row_ror(4)>(x); });
+    if constexpr (L <= 8) v += move(v, [](uint32_t x) { return dpp_u<dpp_row_ror(8)>(x); });
+    auto swap_sum = [&](auto swap) {  // the pair (lane & ~m, lane | m) in that order, for both lanes
+        if constexpr (sizeof(V) == 8) {
+            const uint64_t b = __double_as_longlong(v);
+            const auto lo = swap((uint32_t)b), hi = swap((uint32_t)(b >> 32));
+            const double a = __longlong_as_double((int64_t)(((uint64_t)hi[0] << 32) | lo[0]));
+            const double c = __longlong_as_double((int64_t)(((uint64_t)hi[1] << 32) | lo[1]));
+            return (V)(a + c);
+        } else {
+            const auto r = swap(__float_as_uint(v));
+            return (V)(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+        }
+    };
+    if constexpr (L <= 16)
+        v = swap_sum([](uint32_t x) { return __builtin_amdgcn_permlane16_swap(x, x, false, false); });
+    v = swap_sum([](uint32_t x) { return __builtin_amdgcn_permlane32_swap(x, x, false, false); });
+    return v;
+}
 constexpr int64_t kEpsMinPos = int64_t(1) << 26;
 
 // eps = (a_t - a_0) - t f with each product rounded on its own, as the angle
@@ -190,9 +230,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
 #pragma unroll
-            for (int o = LPR; o < kWave; o <<= 1)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) acc[k][e] += __shfl_xor(acc[k][e], o, kWave);
+            for (int e = 0; e < VEC; ++e) acc[k][e] = sum_lanes_mod<LPR>(acc[k][e]);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) mean[e] = (double)acc[k][e] * ks * inv;
             if (tg == 0) {
