@@ -441,9 +441,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
 // fewer rows the matrix cores still leave the vector units freer than the
 // vector kernel does.  Lane l of a wave works on query row l % 16;
 // kg = l / 16 picks its 8-element slice of each 32-long contraction.
-//   scores  S^T = K Q^T per 16 tokens: K rows come straight from memory into
-//           the A operand (lane: token l%16, 8 dims), Q^T is the B operand kept
-//           in registers.  Q is split as hi + lo bf16 (q = hi + lo to 2^-16),
+//   scores  S^T = K Q^T per 16 tokens: K (A operand, lane: token l%16, 8
+//           dims) is read from a per-wave LDS copy of the tile, which is loaded
+//           like V with whole rows per load instruction (the operand layout
+//           itself would touch 16 rows and half a cache line of each per
+//           instruction); Q^T is the B operand kept in registers.  Q is split as hi + lo bf16 (q = hi + lo to 2^-16),
 //           so the logits keep fp32 accuracy at twice the (cheap) MFMA count.
 //           Lane l receives S[row l%16][tokens 4kg .. 4kg+3] of the 16.
 //   softmax online per row in base 2; each lane holds 8 scores of its row per
@@ -460,7 +462,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
 // codes per instruction); k_scale is folded into Q and v_scale into the
 // partial output.  One 16-byte K load then holds 16 dims, which feed two
 // 32-long contractions: chunk 2c+u takes dims 64c + 16kg + 8u + [0, 8), and Q
-// is laid out the same way.  V codes are widened before they go to LDS.
+// is laid out the same way.  K codes stay codes in LDS and are widened after
+// the operand read; V codes are widened before they go to LDS.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kMfmaRows = 16;
@@ -515,9 +518,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     constexpr int VP = D + 16;           // LDS row pitch of the V tile, in halves (rows 8 banks apart)
     constexpr int VL = kMfmaTile * D / EPL / kWave;  // 16-byte V loads per lane per tile
     static_assert(VL * kWave * EPL == kMfmaTile * D, "V tile split over the wave");
+    // K is loaded the way V is (each load instruction covers whole rows, 1 KB
+    // contiguous) and read back in the A-operand layout from a per-wave LDS
+    // tile of raw elements (FP8 codes are widened after that read)
+    constexpr int KPB = D * (int)sizeof(T) + 16;  // LDS row pitch of the K tile, in bytes
+    static_assert(2 * KL == VL, "K and V tiles take the same loads");
     // first dim of the lane's 8-long slice of contraction chunk c (Q and K alike)
     auto chunk_dim = [&](int c, int kg) { return F8 ? 64 * (c / 2) + 16 * kg + 8 * (c % 2) : 32 * c + 8 * kg; };
     __shared__ uint16_t sm_v[kAttnWaves][kMfmaTile * VP];
+    __shared__ __attribute__((aligned(16))) uint8_t sm_k[kAttnWaves][kMfmaTile * KPB];
     __shared__ float sm_m[kAttnWaves][kMfmaRows], sm_l[kAttnWaves][kMfmaRows];
     __shared__ int sm_bad[kAttnWaves];
 
@@ -564,17 +573,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float mrun = -INFINITY, lpart = 0.f;
 
-    // K and V of tile t (16 tokens of a half never cross a page): K half h,
-    // lane -> token 16h + r16, 16 bytes at dim chunk_dim(c * EPL / 8, kg); V
-    // load i -> token (lane + 64 i) / (D/EPL), 16 bytes at dim
-    // EPL * ((lane + 64 i) % (D/EPL)).  Tokens past the split read the split's
+    // K and V of tile t (16 tokens of a half never cross a page): load i ->
+    // token (lane + 64 i) / (D/EPL), 16 bytes at dim EPL * ((lane + 64 i) %
+    // (D/EPL)), for K and V alike.  Tokens past the split read the split's
     // last token again (in bounds) and are masked out of the softmax.
     // A full tile takes the fast path: each half's page base is wave-uniform
-    // (scalar registers) and every lane adds a fixed 32-bit offset: for K
-    // r16 * D + chunk_dim(0, kg) (later chunks by immediate offsets), for V
-    // load i lane * EPL plus a constant (load i covers 64 / (D/EPL) whole
-    // tokens, all in one half).  Only the split's last tile clamps per lane.
-    const uint32_t k_lane = (uint32_t)(r16 * D + chunk_dim(0, kg));
+    // (scalar registers) and load i adds lane * EPL plus a constant (it covers
+    // 64 / (D/EPL) whole tokens, all in one half).  Only the split's last tile
+    // clamps per lane.
     const uint32_t v_lane = (uint32_t)(lane * EPL);
     constexpr int TPI = kWave / (D / EPL);  // tokens per V load instruction
     static_assert(16 % TPI == 0, "a V load stays inside one half");
@@ -582,19 +588,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
         const int64_t pg = __builtin_amdgcn_readfirstlane(sm_pg[s0 / BT]);
         return (pg * n_kv_heads + g) * (int64_t)BT * D + (int64_t)(s0 % BT) * D;
     };
-    auto load_tile = [&](int t, uint4 (&kb)[2][KL], uint4 (&vb)[VL]) {
+    auto load_tile = [&](int t, uint4 (&kb)[VL], uint4 (&vb)[VL]) {
         if (t * kMfmaTile + kMfmaTile <= n_tok) {
             int64_t base[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) base[h] = half_base(t * kMfmaTile + 16 * h);
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-                for (int c = 0; c < KL; ++c)
-                    kb[h][c] = load_stream16(k_pool + base[h] + k_lane + (chunk_dim(c * EPL / 8, 0) - chunk_dim(0, 0)));
-#pragma unroll
             for (int i = 0; i < VL; ++i) {
                 const int h = i * TPI / 16;
+                kb[i] = load_stream16(k_pool + base[h] + v_lane + (i * TPI - 16 * h) * D);
                 vb[i] = load_stream16(v_pool + base[h] + v_lane + (i * TPI - 16 * h) * D);
             }
             return;
@@ -609,21 +611,26 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             vbase[h] = v_pool + off;
         }
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int tok = min(16 * h + r16, n_tok - 1 - (t * kMfmaTile + 16 * h) + 16 * h);
-#pragma unroll
-            for (int c = 0; c < KL; ++c)
-                kb[h][c] = load_stream16(kbase[h] + (int64_t)(tok - 16 * h) * D + chunk_dim(c * EPL / 8, kg));
-        }
-#pragma unroll
         for (int i = 0; i < VL; ++i) {
             const int idx = lane + kWave * i, x = idx / (D / EPL), ch = idx % (D / EPL);
             const int h = x / 16;
-            const int tok = min(x, n_tok - 1 - t * kMfmaTile);
-            vb[i] = load_stream16(vbase[h] + (int64_t)(tok - 16 * h) * D + EPL * ch);
+            const int64_t off = (int64_t)(min(x, n_tok - 1 - t * kMfmaTile) - 16 * h) * D + EPL * ch;
+            kb[i] = load_stream16(kbase[h] + off);
+            vb[i] = load_stream16(vbase[h] + off);
         }
     };
     uint16_t *my_v = sm_v[wave];
+    uint8_t *my_k = sm_k[wave];
+    // K tile to LDS as loaded: row x at pitch KPB, 16 bytes at 16*ch (the 16
+    // rows of an operand read then start 4 banks apart at d = 128 bf16 and
+    // at 16 distinct 4-bank offsets for FP8)
+    auto stage_k = [&](const uint4 (&kb)[VL]) {
+#pragma unroll
+        for (int i = 0; i < VL; ++i) {
+            const int idx = lane + kWave * i, x = idx / (D / EPL), ch = idx % (D / EPL);
+            *reinterpret_cast<uint4 *>(my_k + x * KPB + 16 * ch) = kb[i];
+        }
+    };
     // V tile to LDS as bf16 (row x, EPL values at EPL*ch); a wave reads only its own tile
     auto stage_v = [&](const uint4 (&vb)[VL]) {
 #pragma unroll
@@ -641,7 +648,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             }
         }
     };
-    auto process = [&](int t, const uint4 (&kb)[2][KL]) {
+    auto process = [&](int t) {
         // scores of the 32 tokens: lane gets row r16, tokens 16h + 4kg + i
         float sc[8];
 #pragma unroll
@@ -649,13 +656,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             f32x4_t st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < KC; ++c) {
+                // the lane's 16 bytes of K row 16h + r16 (FP8: two chunks' codes)
+                const uint4 w = *reinterpret_cast<const uint4 *>(
+                    my_k + (16 * h + r16) * KPB + (int)sizeof(T) * chunk_dim(F8 ? c & ~1 : c, kg));
                 bf16x8_t kk;
-                if constexpr (F8) {
-                    const uint4 w = kb[h][c / 2];
-                    kk = c % 2 == 0 ? fp8x8_to_bf16x8(w.x, w.y) : fp8x8_to_bf16x8(w.z, w.w);
-                } else {
-                    kk = as_bf16x8(kb[h][c]);
-                }
+                if constexpr (F8) kk = c % 2 == 0 ? fp8x8_to_bf16x8(w.x, w.y) : fp8x8_to_bf16x8(w.z, w.w);
+                else kk = as_bf16x8(w);
                 st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qhi[c], st, 0, 0, 0);
                 st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qlo[c], st, 0, 0, 0);
             }
@@ -704,24 +710,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
             acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[mb], 0, 0, 0);
         }
     };
-    // wave w takes tiles w, w + 4, ...; the next tile's loads are in flight
-    // while the current one is processed (its V goes to LDS first, so only
-    // one V tile is held in registers)
+    // wave w takes tiles w, w + 4, ...: the tile's K and V go to LDS, the
+    // next tile's loads are issued into the same registers, then the tile is
+    // processed from LDS while they are in flight
     {
-        uint4 ka[2][KL], kb2[2][KL], vx[VL];
+        uint4 kx[VL], vx[VL];
         int t = wave;
-        if (t < n_tiles) load_tile(t, ka, vx);
+        if (t < n_tiles) load_tile(t, kx, vx);
         while (t < n_tiles) {
+            stage_k(kx);
             stage_v(vx);
             const int t1 = t + kAttnWaves;
-            if (t1 < n_tiles) load_tile(t1, kb2, vx);
-            process(t, ka);
-            if (t1 >= n_tiles) break;
-            stage_v(vx);
-            const int t2 = t1 + kAttnWaves;
-            if (t2 < n_tiles) load_tile(t2, ka, vx);
-            process(t1, kb2);
-            t = t2;
+            if (t1 < n_tiles) load_tile(t1, kx, vx);
+            process(t);
+            t = t1;
         }
     }
     // row sums over the 4 kg lanes
