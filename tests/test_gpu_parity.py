@@ -539,3 +539,27 @@ def test_all_equal_scores_150k(m, k):
     vb = st.view_blocks.cpu().numpy()[0]
     assert vb.tolist() == list(range(k)) + list(range(m, m + 5))
 
+
+@pytest.mark.parametrize("copies", [500, 586])
+def test_over_a_thousand_splits(copies):
+    """A view of 512 distinct pages, each listed `copies` times, gives the same
+    output as the distinct pages alone and a log-sum-exp larger by ln(copies)
+    (every token's weight appears `copies` times in both sums of the softmax).
+    500 and 586 copies make 1,000 and 1,172 splits of 256 pages, so the merge
+    walks far more splits than it preloads."""
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", 512, 0, 2, 1, W.MAX_GROUP, 10)
+    log(f"[case] 512 pages x {copies} copies, 1 KV head, 4 rows")
+    w = W.generate(cfg, 29)
+    distinct = np.random.default_rng(7).permutation(cfg.n_blocks).astype(np.int32)[None]
+    o_ref, l_ref = oracle.view_attention(w.q[0, 0], w.k_pool[0], w.v_pool[0], distinct)
+    vp = torch.from_numpy(np.tile(distinct, (1, copies))).cuda()
+    st = LayerState(cfg, w.k_pool[0], w.v_pool[0], w.block_to_page)
+    qd = torch.from_numpy(np.ascontiguousarray(w.q[0, 0])).cuda()
+    out, lse = st.attend(qd, vp)
+    torch.cuda.synchronize()
+    o1, l1 = out.cpu().numpy().copy(), lse.cpu().numpy().copy()
+    check_attention(o1, l1, o_ref, l_ref + math.log(copies), "bf16")
+    # a second call through the same workspace gives the same bits
+    out, lse = st.attend(qd, vp)
+    torch.cuda.synchronize()
+    assert np.array_equal(o1, out.cpu().numpy()) and np.array_equal(l1, lse.cpu().numpy())
