@@ -97,7 +97,12 @@ __device__ inline float rope_eps(int64_t p0, int t, double f) {
     return (float)((at - a0) - tf);
 }
 
-template <typename T, int D, bool ROPE>
+// EPS: compile the loop that corrects for the rounding of the angle products
+// (blocks at positions of 2^26 or more); it holds about 90 more VGPRs than the
+// plain loop, so launches whose positions are known to stay below 2^26 leave
+// it out.  With ROPE the (cos, sin) table of t * f_j takes block_tokens * D/2
+// float2 of dynamic LDS.
+template <typename T, int D, bool ROPE, bool EPS>
 __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ block_to_page,
     int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens, float k_scale,
@@ -111,13 +116,19 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     constexpr bool F8 = sizeof(T) == 1;
     // exact sums: fp32 for unrotated FP8 codes, fp64 otherwise
     using Acc = typename std::conditional<F8 && !ROPE, float, double>::type;
-    // blocks per step: about 16 loads in flight per lane; the rotation's
-    // per-block cos/sin take registers, so fewer blocks with RoPE
+    // blocks per step: about 16 loads in flight per lane without RoPE; the
+    // rotation's per-block cos/sin take registers, so with RoPE one block per
+    // step (more waves per SIMD instead: at d = 128 the bf16 kernel then holds
+    // 83 VGPRs against 181 with two blocks, and the 1M index takes 0.66 ms
+    // against 0.84), except in the kernel with the rounding correction
     constexpr int BPS0 = 16 / NI > 4 ? 4 : 16 / NI;
-    constexpr int BPS = !ROPE || BPS0 == 1 ? BPS0 : BPS0 / 2;
+    constexpr int BPS = !ROPE || BPS0 == 1 ? BPS0 : (!EPS ? 1 : BPS0 / 2);
     constexpr int RB = ROPE ? BPS : 1, RV = ROPE ? VEC / 2 : 1;  // sizes of the per-block rotation
     __shared__ float tile_buf[kIndexTile * PAD];
-    __shared__ float2 rot_t[ROPE ? kMaxBlockTokens * (D / 2) : 1];  // (cos, sin) of t * f_j
+    // RoPE: (cos, sin) of t * f_j, row t at pitch RP: a wave's reads (rows
+    // tg, pairs lp * VEC/2 + e) then fall on distinct banks two lanes at a time
+    extern __shared__ float2 rot_t[];
+    constexpr int RP = D / 2 + 1;
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int tg = lane / LPR, lp = lane % LPR;
@@ -134,7 +145,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         for (int i = threadIdx.x; i < block_tokens * (D / 2); i += kWaves * kWave) {
             float c, sn;
             rope_cos_sin(i / (D / 2), fr.f[i % (D / 2)], &c, &sn);
-            rot_t[i] = make_float2(c, sn);
+            rot_t[(i / (D / 2)) * RP + i % (D / 2)] = make_float2(c, sn);
         }
         __syncthreads();
     }
@@ -189,7 +200,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                     float2 rt[RV];
                     if constexpr (ROPE) {
 #pragma unroll
-                        for (int e = 0; e < HV; ++e) rt[e] = rot_t[t * (D / 2) + j0 + e];
+                        for (int e = 0; e < HV; ++e) rt[e] = rot_t[t * RP + j0 + e];
                     }
 #pragma unroll
                     for (int k = 0; k < BPS; ++k) {
@@ -223,10 +234,14 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
             for (int k = 0; k < BPS; ++k) any_far |= far[k];
         }
-        if (any_far)  // wave-uniform
-            sum_tokens(std::true_type{});
-        else
+        if constexpr (EPS) {
+            if (any_far)  // wave-uniform
+                sum_tokens(std::true_type{});
+            else
+                sum_tokens(std::false_type{});
+        } else {
             sum_tokens(std::false_type{});
+        }
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
 #pragma unroll
@@ -273,11 +288,20 @@ hipError_t launch_t(int n_kv_heads, int block_tokens, float k_scale, const void 
     RopeFreqs f{};
     if (rope) {
         f = *fr;
-        hipLaunchKernelGGL((build_index_kernel<T, D, true>), grid, dim3(kWaves * kWave), 0, stream,
-                           static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
-                           n_kv_heads, block_tokens, k_scale, index, block_pos, f);
+        const size_t lds = sizeof(float2) * (size_t)block_tokens * (D / 2 + 1);
+        // default positions b * block_tokens all below 2^26: the rounding
+        // correction is never taken, so leave it out of the kernel
+        const bool near = block_pos == nullptr && ((int64_t)first_block + n_blocks) * block_tokens <= kEpsMinPos;
+        if (near)
+            hipLaunchKernelGGL((build_index_kernel<T, D, true, false>), grid, dim3(kWaves * kWave), lds, stream,
+                               static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
+                               n_kv_heads, block_tokens, k_scale, index, block_pos, f);
+        else
+            hipLaunchKernelGGL((build_index_kernel<T, D, true, true>), grid, dim3(kWaves * kWave), lds, stream,
+                               static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
+                               n_kv_heads, block_tokens, k_scale, index, block_pos, f);
     } else {
-        hipLaunchKernelGGL((build_index_kernel<T, D, false>), grid, dim3(kWaves * kWave), 0, stream,
+        hipLaunchKernelGGL((build_index_kernel<T, D, false, false>), grid, dim3(kWaves * kWave), 0, stream,
                            static_cast<const T *>(k_pool), n_pages, block_to_page, first_block, n_blocks,
                            n_kv_heads, block_tokens, k_scale, index, block_pos, f);
     }
