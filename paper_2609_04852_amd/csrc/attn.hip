@@ -513,11 +513,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     constexpr bool F8 = sizeof(T) == 1;
     constexpr int EPL = 16 / sizeof(T);  // elements per 16-byte load
     constexpr int KC = D / 32;           // 32-long chunks of the head dimension (scores)
-    constexpr int KL = F8 ? KC / 2 : KC; // 16-byte K loads per lane per 16-token half
+    constexpr int KL = F8 ? KC / 2 : KC; // 16-byte K operand reads per lane per 16-token half
     constexpr int MB = D / 16;           // 16-dim blocks of the output
     constexpr int VP = D + 16;           // LDS row pitch of the V tile, in halves (rows 8 banks apart)
-    constexpr int VL = kMfmaTile * D / EPL / kWave;  // 16-byte V loads per lane per tile
-    static_assert(VL * kWave * EPL == kMfmaTile * D, "V tile split over the wave");
+    constexpr int VL = kMfmaTile * D / EPL / kWave;  // 16-byte loads per lane per tile, of K and of V
+    static_assert(VL * kWave * EPL == kMfmaTile * D, "K and V tiles split over the wave");
     // K is loaded the way V is (each load instruction covers whole rows, 1 KB
     // contiguous) and read back in the A-operand layout from a per-wave LDS
     // tile of raw elements (FP8 codes are widened after that read)
@@ -582,8 +582,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     // 64 / (D/EPL) whole tokens, all in one half).  Only the split's last tile
     // clamps per lane.
     const uint32_t v_lane = (uint32_t)(lane * EPL);
-    constexpr int TPI = kWave / (D / EPL);  // tokens per V load instruction
-    static_assert(16 % TPI == 0, "a V load stays inside one half");
+    constexpr int TPI = kWave / (D / EPL);  // tokens per load instruction
+    static_assert(16 % TPI == 0, "a load instruction stays inside one half");
     auto half_base = [&](int s0) -> int64_t {  // s0: first token of a half, wave-uniform, < n_tok
         const int64_t pg = __builtin_amdgcn_readfirstlane(sm_pg[s0 / BT]);
         return (pg * n_kv_heads + g) * (int64_t)BT * D + (int64_t)(s0 % BT) * D;
