@@ -116,6 +116,8 @@ SHAPES = [
     # the largest KV head count the library takes (64), no grouping
     (64, 64, 64, 16, "bf16", 200, 1, 2, 1, W.MAX_GROUP, 30),
     (64, 128, 128, 32, "bf16", 150, 0, 3, 2, W.MEAN_ALL, 25),
+    # 4 sink blocks, G = 8 (8 rows per KV head on the matrix cores)
+    (4, 32, 128, 16, "bf16", 800, 4, 6, 1, W.MEAN_ALL, 90),
 ]
 
 
