@@ -116,12 +116,14 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     constexpr bool F8 = sizeof(T) == 1;
     // exact sums: fp32 for unrotated FP8 codes, fp64 otherwise
     using Acc = typename std::conditional<F8 && !ROPE, float, double>::type;
-    // blocks per step: about 16 loads in flight per lane without RoPE; the
+    // blocks per step.  Without RoPE two (8 loads of 16 bytes in flight per
+    // lane for bf16 at d = 128, occupancy 4; four blocks held 168 VGPRs at
+    // occupancy 3 and were 2-4% slower, eight were slower still).  The
     // rotation's per-block cos/sin take registers, so with RoPE one block per
-    // step (more waves per SIMD instead: at d = 128 the bf16 kernel then holds
-    // 83 VGPRs against 181 with two blocks, and the 1M index takes 0.66 ms
-    // against 0.84), except in the kernel with the rounding correction
-    constexpr int BPS0 = 16 / NI > 4 ? 4 : 16 / NI;
+    // step (at d = 128 the bf16 kernel then holds 83 VGPRs against 181 with
+    // two blocks, and the 1M index takes 0.66 ms against 0.84), except in the
+    // kernel with the rounding correction
+    constexpr int BPS0 = !ROPE ? 2 : (16 / NI > 4 ? 4 : 16 / NI);
     constexpr int BPS = !ROPE || BPS0 == 1 ? BPS0 : (!EPS ? 1 : BPS0 / 2);
     constexpr int RB = ROPE ? BPS : 1, RV = ROPE ? VEC / 2 : 1;  // sizes of the per-block rotation
     __shared__ float tile_buf[kIndexTile * PAD];
