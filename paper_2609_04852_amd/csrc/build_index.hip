@@ -152,6 +152,21 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         __syncthreads();
     }
 
+    // The page (and RoPE position) of each of the wave's kIndexTile / kWaves
+    // slots, one clamped load per lane up front: the steps below take them
+    // from this lane instead of a dependent memory round trip each.
+    constexpr int kSlots = kIndexTile / kWaves;
+    static_assert(kSlots <= kWave, "one slot per lane");
+    int32_t slot_page = -1;
+    int64_t slot_pos = 0;
+    {
+        const int64_t b = b_tile0 + wave + (int64_t)kWaves * lane;
+        const bool in = lane < kSlots && b >= b_lo && b < b_hi;
+        const int64_t bc = in ? b : b_lo;
+        const int32_t pg = block_to_page[bc];
+        slot_page = in ? pg : -1;
+        if constexpr (ROPE) slot_pos = block_pos ? block_pos[bc] : b * (int64_t)block_tokens;
+    }
     // wave w reduces tile slots w, w+4, w+8, ... (BPS at a time)
     for (int s0 = wave; s0 < kIndexTile; s0 += kWaves * BPS) {
         Acc acc[BPS][VEC];
@@ -164,8 +179,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
+            const int m = (s0 - wave) / kWaves + k;  // the block's slot (wave-uniform)
             const bool in = b >= b_lo && b < b_hi;
-            const int64_t page = in ? block_to_page[b] : -1;
+            const int64_t page = in ? __builtin_amdgcn_readlane(slot_page, m) : -1;
             ok[k] = in && page >= 0 && page < n_pages;
             // a block outside the range or without a valid page reads page 0
             // (in bounds) and is written as NaN
@@ -174,7 +190,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[k][e] = 0;
             if constexpr (ROPE) {
-                p0[k] = block_pos && ok[k] ? block_pos[b] : b * (int64_t)block_tokens;
+                const int64_t pm = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(slot_pos >> 32), m) << 32) |
+                                             (uint32_t)__builtin_amdgcn_readlane((int)slot_pos, m));
+                p0[k] = block_pos && ok[k] ? pm : b * (int64_t)block_tokens;
                 far[k] = !(p0[k] > -kEpsMinPos && p0[k] + block_tokens <= kEpsMinPos);
 #pragma unroll
                 for (int e = 0; e < HV; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
