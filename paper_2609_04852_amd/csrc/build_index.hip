@@ -131,6 +131,10 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     // tg, pairs lp * VEC/2 + e) then fall on distinct banks two lanes at a time
     extern __shared__ float2 rot_t[];
     constexpr int RP = D / 2 + 1;
+    // RoPE: (cos, sin) of p0 * f_j for every pair of the wave's current
+    // blocks, computed one pair per lane and read back by the TG lanes that
+    // hold the pair on their rows (each of which computed it before)
+    __shared__ float2 rot_0[ROPE ? kWaves * BPS * (D / 2) : 1];
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int tg = lane / LPR, lp = lane % LPR;
@@ -194,8 +198,18 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                                              (uint32_t)__builtin_amdgcn_readlane((int)slot_pos, m));
                 p0[k] = block_pos && ok[k] ? pm : b * (int64_t)block_tokens;
                 far[k] = !(p0[k] > -kEpsMinPos && p0[k] + block_tokens <= kEpsMinPos);
+                float2 *r0 = rot_0 + (wave * BPS + k) * (D / 2);
+                for (int j = lane; j < D / 2; j += kWave) {
+                    float c, sn;
+                    rope_cos_sin(p0[k], fr.f[j], &c, &sn);
+                    r0[j] = make_float2(c, sn);
+                }
 #pragma unroll
-                for (int e = 0; e < HV; ++e) rope_cos_sin(p0[k], fr.f[j0 + e], &c0[k][e], &s0v[k][e]);
+                for (int e = 0; e < HV; ++e) {
+                    const float2 cs = r0[j0 + e];
+                    c0[k][e] = cs.x;
+                    s0v[k][e] = cs.y;
+                }
             }
         }
         // the token loop, compiled with and without the rounding correction
