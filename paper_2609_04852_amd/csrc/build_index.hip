@@ -243,9 +243,15 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                         if constexpr (ROPE) {
 #pragma unroll
                             for (int e = 0; e < HV; ++e) {  // pair j0 + e: v[e] and v[HV + e]
-                                float c = c0[k][e] * rt[e].x - s0v[k][e] * rt[e].y;
-                                float sn = s0v[k][e] * rt[e].x + c0[k][e] * rt[e].y;
+                                // with the correction: the token's whole turn by
+                                // (p0 + t) f_j; without it only the turn by t f_j,
+                                // the block's common turn by p0 f_j being applied
+                                // to the sum afterwards (rotations compose)
+                                float c = rt[e].x, sn = rt[e].y;
                                 if constexpr (decltype(with_eps)::value) {
+                                    const float ct = c;
+                                    c = c0[k][e] * ct - s0v[k][e] * sn;
+                                    sn = s0v[k][e] * ct + c0[k][e] * sn;
                                     const float eps = rope_eps(p0[k], t, fr.f[j0 + e]);
                                     const float cc = c;
                                     c = cc - sn * eps;
@@ -276,12 +282,23 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         } else {
             sum_tokens(std::false_type{});
         }
+        const bool turn_sum = !(EPS && any_far);  // RoPE: the sums still owe the turn by p0 f_j
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[k][e] = sum_lanes_mod<LPR>(acc[k][e]);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) mean[e] = (double)acc[k][e] * ks * inv;
+            if constexpr (ROPE) {
+                if (turn_sum) {
+#pragma unroll
+                    for (int e = 0; e < HV; ++e) {
+                        const double lo = mean[e], hi = mean[HV + e], c = c0[k][e], sn = s0v[k][e];
+                        mean[e] = lo * c + hi * sn;
+                        mean[HV + e] = hi * c - lo * sn;
+                    }
+                }
+            }
             if (tg == 0) {
                 float *dst = tile_buf + (s0 + k * kWaves) * PAD;
                 if constexpr (ROPE) {  // dims j0 + e and D/2 + j0 + e
