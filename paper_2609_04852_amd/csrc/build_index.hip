@@ -24,12 +24,18 @@ namespace {
 
 constexpr int kWaves = 4;
 
+// 4-byte load of raw keys read once (the non-temporal hint of load_stream16)
+template <typename T>
+__device__ inline uint32_t load_stream4(const T *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const unsigned int *>(p));
+}
+
 // ROPE: the stored keys carry RoPE (rotate-half form) at positions
 // block_pos[b] + t (block_pos NULL: b * block_tokens + t); each token row is
 // turned back to position 0 before it enters the sum (Sec. 4.3: the index is
 // built from position-independent keys).  A lane then reads its row as two
-// 8-byte pieces, the VEC/2 dims [j0, j0 + VEC/2) and the matching dims of the
-// other half, so that it holds both members of its pairs.
+// pieces (8 bytes; 4 for FP8 codes), the VEC/2 dims [j0, j0 + VEC/2) and the
+// matching dims of the other half, so that it holds both members of its pairs.
 // The angle of token t is the fp64 product a_t = (p0 + t) f_j (as in the
 // definition), turned into a rotation without a sin/cos per token: with
 // a_0 = p0 f_j (its cos/sin taken once per block and pair, the angle reduced
@@ -107,13 +113,17 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     const T *__restrict__ k_pool, int64_t n_pages, const int32_t *__restrict__ block_to_page,
     int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens, float k_scale,
     float *__restrict__ index, const int64_t *__restrict__ block_pos, RopeFreqs fr) {
-    constexpr int VEC = Vec16<T>::N;  // elements per lane per row
+    constexpr bool F8 = sizeof(T) == 1;
+    // elements per lane per row.  Rotated FP8 keys take 8 (as bf16 does), not
+    // the 16 of a 16-byte load: the fp64 sums of a lane's elements are then
+    // exchanged between 4 lanes of a row group instead of 8, over half as
+    // many elements (a third of the cross-lane work)
+    constexpr int VEC = F8 && ROPE ? 8 : Vec16<T>::N;
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
     constexpr int NI = 16 / TG;       // instructions per 16 tokens
     static_assert(NI * TG == 16, "16 tokens split over whole instructions");
     constexpr int PAD = D + 4;        // LDS row stride (floats): conflict-free column reads
-    constexpr bool F8 = sizeof(T) == 1;
     // exact sums: fp32 for unrotated FP8 codes, fp64 otherwise
     using Acc = typename std::conditional<F8 && !ROPE, float, double>::type;
     // blocks per step.  Without RoPE two (8 loads of 16 bytes in flight per
@@ -221,7 +231,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
                     for (int i = 0; i < NI; ++i) {
                         const T *row = base[k] + (int64_t)(t0 + tg + TG * i) * D;
-                        if constexpr (ROPE) {
+                        if constexpr (ROPE && F8) {
+                            raw[k][i] = make_uint4(load_stream4(row), load_stream4(row + D / 2), 0u, 0u);
+                        } else if constexpr (ROPE) {
                             const uint2 lo = load_stream8(row), hi = load_stream8(row + D / 2);
                             raw[k][i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
                         } else {
@@ -239,7 +251,18 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
                     for (int k = 0; k < BPS; ++k) {
                         float v[VEC];
-                        Vec16<T>::decode(raw[k][i], v);
+                        if constexpr (ROPE && F8) {  // 4 codes of each half
+                            const uint32_t w[2] = {raw[k][i].x, raw[k][i].y};
+#pragma unroll
+                            for (int h = 0; h < 2; ++h) {
+                                const f32x2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8(w[h], false);
+                                const f32x2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8(w[h], true);
+                                v[4 * h] = lo[0]; v[4 * h + 1] = lo[1];
+                                v[4 * h + 2] = hi[0]; v[4 * h + 3] = hi[1];
+                            }
+                        } else {
+                            Vec16<T>::decode(raw[k][i], v);
+                        }
                         if constexpr (ROPE) {
 #pragma unroll
                             for (int e = 0; e < HV; ++e) {  // pair j0 + e: v[e] and v[HV + e]
