@@ -114,11 +114,11 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
     int32_t first_block, int32_t n_blocks, int n_kv_heads, int block_tokens, float k_scale,
     float *__restrict__ index, const int64_t *__restrict__ block_pos, RopeFreqs fr) {
     constexpr bool F8 = sizeof(T) == 1;
-    // elements per lane per row.  Rotated FP8 keys take 8 (as bf16 does), not
-    // the 16 of a 16-byte load: the fp64 sums of a lane's elements are then
-    // exchanged between 4 lanes of a row group instead of 8, over half as
-    // many elements (a third of the cross-lane work)
-    constexpr int VEC = F8 && ROPE ? 8 : Vec16<T>::N;
+    // elements per lane per row.  FP8 keys take 8 (as bf16 does), not the 16
+    // of a 16-byte load: the sums of a lane's elements are then exchanged
+    // between 4 lanes of a row group instead of 8, over half as many elements
+    // (a third of the cross-lane work)
+    constexpr int VEC = F8 ? 8 : Vec16<T>::N;
     constexpr int LPR = D / VEC;      // lanes per token row
     constexpr int TG = kWave / LPR;   // token rows per wave instruction
     constexpr int NI = 16 / TG;       // instructions per 16 tokens
@@ -233,6 +233,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                         const T *row = base[k] + (int64_t)(t0 + tg + TG * i) * D;
                         if constexpr (ROPE && F8) {
                             raw[k][i] = make_uint4(load_stream4(row), load_stream4(row + D / 2), 0u, 0u);
+                        } else if constexpr (F8) {
+                            const uint2 w = load_stream8(row);
+                            raw[k][i] = make_uint4(w.x, w.y, 0u, 0u);
                         } else if constexpr (ROPE) {
                             const uint2 lo = load_stream8(row), hi = load_stream8(row + D / 2);
                             raw[k][i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
 #pragma unroll
                     for (int k = 0; k < BPS; ++k) {
                         float v[VEC];
-                        if constexpr (ROPE && F8) {  // 4 codes of each half
+                        if constexpr (F8) {  // 8 codes in two words (RoPE: 4 of each half)
                             const uint32_t w[2] = {raw[k][i].x, raw[k][i].y};
 #pragma unroll
                             for (int h = 0; h < 2; ++h) {
