@@ -446,21 +446,21 @@ def main():
             st.select(qs[l:l + 1], with_scores=False)
             st.attend(qs[l])
 
-    def graph_rate(n_graph, rotate, steps):
-        """ms per step replaying n_graph captured steps (one graph replay runs them all)."""
+    def graph_rate(rotate, steps):
+        """ms per step of exactly `steps` steps captured in one graph (step i on
+        query set i mod n_sets and replica i mod n_rep), replayed once untimed
+        and then once timed."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            for i in range(n_graph):
+            for i in range(steps):
                 step(i, rotate=rotate)
         g.replay()
         torch.cuda.synchronize()
-        reps_ = max(1, steps // n_graph)
-        print(f"[bench] timing {reps_ * n_graph} steps by graph replay", file=sys.stderr, flush=True)
+        print(f"[bench] timing {steps} steps by graph replay", file=sys.stderr, flush=True)
         t0 = time.perf_counter()
-        for _ in range(reps_):
-            g.replay()
+        g.replay()
         torch.cuda.synchronize()
-        return g, reps_ * n_graph, (time.perf_counter() - t0) * 1000.0 / (reps_ * n_graph)
+        return g, steps, (time.perf_counter() - t0) * 1000.0 / steps
 
     for i in range(max(args.warmup, n_rep)):
         step(i)
@@ -486,9 +486,9 @@ def main():
     n_steps, ms_per_step = args.steps, eager_ms
     graph = None
     if args.graph:
-        # the same steps (every query set on every replica) captured once and
-        # replayed: every replay runs the whole selection and attention again
-        graph, n_steps, ms_per_step = graph_rate(int(np.lcm(n_sets, n_rep)), True, args.steps)
+        # the same K steps captured in one graph and replayed: the timed replay
+        # runs every step's whole selection and attention again
+        graph, n_steps, ms_per_step = graph_rate(True, args.steps)
     cache = None
     if n_rep > 1:
         # the same steps on replica 0 only: the "hot" rate, with the pools and
@@ -498,7 +498,7 @@ def main():
             step(i, rotate=False)
         torch.cuda.synchronize()
         hot_eager = (time.perf_counter() - t0) * 1000.0 / args.steps
-        hot = graph_rate(n_sets, False, args.steps)[2] if args.graph else hot_eager
+        hot = graph_rate(False, args.steps)[2] if args.graph else hot_eager
         cache = {"replicas": n_rep, "bytes_rotated_over": n_rep * footprint,
                  "rotated_ms_per_step": round(ms_per_step, 5), "hot_ms_per_step": round(hot, 5),
                  "hot_eager_ms_per_step": round(hot_eager, 5)}

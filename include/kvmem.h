@@ -101,8 +101,9 @@ typedef enum {
     KVMEM_REDUCE_MAX_GROUP = 1
 } kvmem_reduce;
 
-/* Model geometry shared by all calls.  Supported: Hkv a power of two <= 64,
- * G = Hq/Hkv with G * n_q <= 16, d in {64, 128}, Bt in {16, 32, 64}. */
+/* Model geometry shared by all calls.  Supported: 1 <= Hkv <= 64, any
+ * G = Hq/Hkv with G * n_q <= 4096 query rows per KV head (every call), d in
+ * {64, 128}, Bt in {16, 32, 64}; anything else returns KVMEM_ERR_UNSUPPORTED. */
 typedef struct {
     int32_t n_kv_heads;   /* Hkv */
     int32_t n_q_heads;    /* Hq */

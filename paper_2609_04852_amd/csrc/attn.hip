@@ -2,7 +2,7 @@
 // Sec. 5.3): split-K flash-decode plus an exact log-sum-exp merge.
 //
 // Kernels, by shape (launch_bt picks one; every one writes the same partials):
-//   attn_mfma16        bf16 K/V with 4 to 47 query rows per KV head, and FP8
+//   attn_mfma16        bf16 K/V with 3 to 47 query rows per KV head, and FP8
 //                      below 48 rows: both products on the matrix cores
 //   attn_mfma_rows     48 or more rows (bf16, FP8): groups of 16-row waves
 //                      share each K/V tile through LDS
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     }
 }
 
-// MFMA path for bf16 K/V with 4 or more query rows per KV head (e.g. 4 GQA
+// MFMA path for bf16 K/V with 3 or more query rows per KV head (e.g. 4 GQA
 // heads x 4 query tokens), in tiles of 16 rows (a partial last tile is padded
 // with zero queries that are never written).  At 16 rows the step does 16
 // flops per K/V byte, more than the vector units sustain at full HBM rate, so
@@ -1114,9 +1114,9 @@ hipError_t launch_bt(const AttnPlan &p, const float *q, const void *k, const voi
         return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
     } else {
         if constexpr (std::is_same<T, uint16_t>::value) {
-            // bf16 with 4 or more rows per KV head: matrix cores (rows padded to 16)
+            // bf16 with 3 or more rows per KV head: matrix cores (rows padded to 16)
             if (rows >= kRowsLds) return launch_mfma_rows<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
-            if (rows >= 4) return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
+            if (rows >= 3) return launch_mfma16<T, D, BT>(p, q, k, v, n_pages, vp, qscale, part, stream);
         }
         if constexpr (D / Vec16<T>::N == 16) {
             if (rows % 8 == 0) return launch_row16<T, D, BT, 8>(p, q, k, v, n_pages, vp, qscale, part, stream);

@@ -52,7 +52,10 @@ __device__ inline uint32_t load_stream4(const T *p) {
 // (cos eps = 1 - eps^2/2, and eps stays below an fp64 ulp of the angle: 2.4e-4
 // rad even at positions of 2^40).  That is sixteen to sixty-four times fewer
 // sin/cos than one per token, at about two fp32 ulps of the cos and sin.
-// Below kEpsMinPos (2^26) eps is under 1.5e-8 rad and is left out.
+// Below kEpsMinPos (2^26) eps is under 1.5e-8 rad and is left out.  From
+// kDirectMinPos (2^42) on, eps reaches 5e-4 rad and its dropped second-order
+// term (and, past 2^53, the inexact difference a_t - a_0) would show, so such
+// blocks take the cos/sin of every token's own angle a_t instead.
 //
 // Every block_tokens is a multiple of 16, so a wave reads a block 16 tokens
 // at a time: NI = 16 / TG loads per lane, all issued before the first sum,
@@ -100,6 +103,7 @@ __device__ inline V sum_lanes_mod(V v) {
     return v;
 }
 constexpr int64_t kEpsMinPos = int64_t(1) << 26;
+constexpr int64_t kDirectMinPos = int64_t(1) << 42;
 
 // eps = (a_t - a_0) - t f with each product rounded on its own, as the angle
 // a_t = (p0 + t) f is defined (a fused multiply-add would skip a rounding)
@@ -197,7 +201,8 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
         const T *base[BPS];
         float c0[RB][RV], s0v[RB][RV];  // cos, sin of a_0 = p0 * f_j for the lane's pairs
         int64_t p0[RB];
-        bool far[RB];  // positions reach kEpsMinPos: correct for the rounding of the products
+        bool far[RB];   // positions reach kEpsMinPos: correct for the rounding of the products
+        bool vfar[RB];  // positions reach kDirectMinPos: every token's own cos/sin
 #pragma unroll
         for (int k = 0; k < BPS; ++k) {
             const int64_t b = b_tile0 + s0 + k * kWaves;
@@ -216,6 +221,7 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                                              (uint32_t)__builtin_amdgcn_readlane((int)slot_pos, m));
                 p0[k] = block_pos && ok[k] ? pm : b * (int64_t)block_tokens;
                 far[k] = !(p0[k] > -kEpsMinPos && p0[k] + block_tokens <= kEpsMinPos);
+                vfar[k] = !(p0[k] > -kDirectMinPos && p0[k] + block_tokens <= kDirectMinPos);
                 float2 *r0 = rot_0 + (wave * BPS + k) * (D / 2);
                 for (int j = lane; j < D / 2; j += kWave) {
                     float c, sn;
@@ -230,8 +236,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                 }
             }
         }
-        // the token loop, compiled with and without the rounding correction
-        auto sum_tokens = [&](auto with_eps) {
+        // the token loop, compiled without and with the rounding correction
+        // (mode 0, 1) and with every token's own cos/sin (mode 2)
+        auto sum_tokens = [&](auto mode) {
             for (int t0 = 0; t0 < block_tokens; t0 += 16) {
                 uint4 raw[BPS][NI];
 #pragma unroll
@@ -282,7 +289,9 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                                 // the block's common turn by p0 f_j being applied
                                 // to the sum afterwards (rotations compose)
                                 float c = rt[e].x, sn = rt[e].y;
-                                if constexpr (decltype(with_eps)::value) {
+                                if constexpr (decltype(mode)::value == 2) {
+                                    rope_cos_sin(p0[k] + t, fr.f[j0 + e], &c, &sn);
+                                } else if constexpr (decltype(mode)::value == 1) {
                                     const float ct = c;
                                     c = c0[k][e] * ct - s0v[k][e] * sn;
                                     sn = s0v[k][e] * ct + c0[k][e] * sn;
@@ -303,18 +312,24 @@ __global__ __launch_bounds__(kWaves *kWave) void build_index_kernel(
                 }
             }
         };
-        bool any_far = false;
+        bool any_far = false, any_vfar = false;
         if constexpr (ROPE) {
 #pragma unroll
-            for (int k = 0; k < BPS; ++k) any_far |= far[k];
+            for (int k = 0; k < BPS; ++k) {
+                any_far |= far[k];
+                any_vfar |= vfar[k];
+            }
         }
+        using Plain = std::integral_constant<int, 0>;
         if constexpr (EPS) {
-            if (any_far)  // wave-uniform
-                sum_tokens(std::true_type{});
+            if (any_vfar)  // wave-uniform
+                sum_tokens(std::integral_constant<int, 2>{});
+            else if (any_far)
+                sum_tokens(std::integral_constant<int, 1>{});
             else
-                sum_tokens(std::false_type{});
+                sum_tokens(Plain{});
         } else {
-            sum_tokens(std::false_type{});
+            sum_tokens(Plain{});
         }
         const bool turn_sum = !(EPS && any_far);  // RoPE: the sums still owe the turn by p0 f_j
 #pragma unroll

@@ -30,7 +30,6 @@ kvmem_status ok() {
     return KVMEM_OK;
 }
 
-bool pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 kvmem_status check_geom(const kvmem_geom *g) {
@@ -38,9 +37,8 @@ kvmem_status check_geom(const kvmem_geom *g) {
     if (g->n_kv_heads <= 0 || g->n_q_heads <= 0 || g->n_q_heads % g->n_kv_heads != 0)
         return fail(KVMEM_ERR_SHAPE, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
                     g->n_q_heads, g->n_kv_heads);
-    if (!pow2(g->n_kv_heads) || g->n_kv_heads > 64)
-        return fail(KVMEM_ERR_UNSUPPORTED, "n_kv_heads %d: a power of two <= 64 is required",
-                    g->n_kv_heads);
+    if (g->n_kv_heads > 64)
+        return fail(KVMEM_ERR_UNSUPPORTED, "n_kv_heads %d: at most 64 are supported", g->n_kv_heads);
     if (g->head_dim != 64 && g->head_dim != 128)
         return fail(KVMEM_ERR_UNSUPPORTED, "head_dim %d: 64 or 128 is required", g->head_dim);
     if (g->block_tokens != 16 && g->block_tokens != 32 && g->block_tokens != 64)
@@ -95,11 +93,10 @@ kvmem_status make_select_plan(const kvmem_geom *g, int32_t n_layers, int32_t n_q
     if (mode != KVMEM_REDUCE_MEAN_ALL && mode != KVMEM_REDUCE_MAX_GROUP)
         return fail(KVMEM_ERR_SHAPE, "mode %d is not a kvmem_reduce value", mode);
     const int group = g->n_q_heads / g->n_kv_heads;
+    if ((int64_t)group * n_q > kvmem::kRowsMaxPerHead)
+        return fail(KVMEM_ERR_UNSUPPORTED, "G * n_q_tokens = %lld: at most %d query rows per KV head",
+                    (long long)group * n_q, kvmem::kRowsMaxPerHead);
     const int rows = group * n_q;
-    if (!((pow2(rows) && rows <= 16) || (rows % 16 == 0 && rows <= kvmem::kRowsMaxPerHead)))
-        return fail(KVMEM_ERR_UNSUPPORTED,
-                    "G * n_q_tokens = %d: scoring needs a power of two <= 16 or a multiple of 16 <= %d", rows,
-                    kvmem::kRowsMaxPerHead);
     int32_t k_eff = 0, n_view = 0;
     st = plan_view(g, n_blocks, n_sink, n_recent, model_ctx, gpu_kv, &k_eff, &n_view);
     if (st != KVMEM_OK) return st;

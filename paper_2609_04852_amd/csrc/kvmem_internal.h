@@ -27,9 +27,13 @@ __host__ __device__ inline int64_t index_layer_floats(int64_t n_blocks, int n_kv
 // ---- select ------------------------------------------------------------
 // Index tiles scored by one workgroup of the vector logit kernel (one per
 // wave), of the 16-row kernel (each wave takes one 16-block group of each),
-// and of the kernel for more rows.
+// and of the kernel for more rows.  Up to kScoreVectorRows query rows per KV
+// head are scored on the vector units, 9 to 16 on the 16-row matrix-core
+// kernel (rows past the head's count padded with zero queries), more by
+// 16-row chunks.
 constexpr int kScoreTilesPerGroup = 4;
 constexpr int kMfma16Tiles = 1;
+constexpr int kScoreVectorRows = 8;
 // More than 16 query rows per KV head (a recall point's prefill query): one
 // workgroup per index tile runs every row of its (layer, KV head) in chunks of
 // 16 on the matrix cores; the block relevance then sums the rows in
@@ -78,7 +82,8 @@ inline void plan_select_layout(SelectPlan &p) {
     p.n_rows = p.n_layers * p.n_q * p.n_q_heads;
     p.tile_lo = p.n_sink / kIndexTile;
     p.n_tiles = (int)index_tiles(p.n_blocks - p.n_recent) - p.tile_lo;
-    p.tiles_per_part = p.rows_per_head > 16 ? 1 : p.rows_per_head == 16 ? kMfma16Tiles : kScoreTilesPerGroup;
+    p.tiles_per_part = p.rows_per_head > 16 ? 1 : p.rows_per_head > kScoreVectorRows ? kMfma16Tiles
+                                                                                   : kScoreTilesPerGroup;
     p.n_parts = (p.n_tiles + p.tiles_per_part - 1) / p.tiles_per_part;
     {
         const int nr = p.mode == 0 ? p.n_rows : p.n_q * p.group;  // logit rows behind one relevance value

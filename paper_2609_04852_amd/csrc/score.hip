@@ -96,7 +96,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
     }
 }
 
-// 16 query rows per KV head (GQA heads x query tokens): the dot products run
+// 9 to 16 query rows per KV head (GQA heads x query tokens; a tile of 16 rows
+// whose rows past the head's count are zero queries): the dot products run
 // on the fp64 matrix cores (v_mfma_f64_16x16x4f64).  The fp32 inputs widen
 // exactly, their products are exact in fp64 and the sums barely round, so the
 // logit is the fp32 rounding of the exact dot product (the vector kernel's
@@ -128,7 +129,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r16 = lane % 16, kg = lane / 16;
     const int g = blockIdx.y, l = blockIdx.z, gb = wave;
-    const int64_t qrow = ((int64_t)l * n_q + r16 / group) * n_q_heads + g * group + r16 % group;
+    // the head's rows (9 to 16): lanes of rows past them hold zero queries
+    // (a copy of the last row's address, never written)
+    const int rows = group * n_q;
+    const bool row_ok = r16 < rows;
+    const int rr = row_ok ? r16 : rows - 1;
+    const int64_t qrow = ((int64_t)l * n_q + rr / group) * n_q_heads + g * group + rr % group;
     const int64_t tiles_per_layer = index_tiles(n_blocks);
 
     // the group's loads of every tile of the workgroup first (a tile past the
@@ -148,7 +154,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
         const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
-        qv[c][0] = v.x; qv[c][1] = v.y; qv[c][2] = v.z; qv[c][3] = v.w;
+        qv[c][0] = row_ok ? v.x : 0.f; qv[c][1] = row_ok ? v.y : 0.f;
+        qv[c][2] = row_ok ? v.z : 0.f; qv[c][3] = row_ok ? v.w : 0.f;
     }
     __builtin_amdgcn_sched_barrier(0);  // keep every load in flight together
     float s[NT][4];  // tile t, row r16, block 16 * gb + kg + 4i
@@ -175,7 +182,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
         for (int i = 0; i < 4; ++i) {
             int64_t c;
             const bool ok = valid(t, i, c);
-            if (ok) logits[qrow * cand_stride + c] = s[t][i];
+            if (ok && row_ok) logits[qrow * cand_stride + c] = s[t][i];
             mx = fmaxf(mx, ok ? s[t][i] : -INFINITY);
         }
     mx = fmaxf(mx, shfl_xor_f(mx, 16));
@@ -197,7 +204,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
         sm_s[wave][r16] = e;
     }
     __syncthreads();
-    if ((int)threadIdx.x < RH) {
+    if ((int)threadIdx.x < rows) {
         const int r = threadIdx.x;
         const int64_t qr = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
         float m = sm_m[0][r];
@@ -213,7 +220,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
 }
 
 // More than 16 query rows per KV head (a recall point: the prefill's query
-// tokens x the group's heads).  The scoring is then a dense contraction,
+// tokens x the group's heads; a ragged last 16-row chunk is padded with zero
+// queries that are never written).  The scoring is then a dense contraction,
 // S = Q index^T, run on the fp64 matrix cores for the same reason as above.
 // One workgroup per (index tile, KV head, layer): the tile's 64 x D floats are
 // staged in LDS once and serve every row of that (layer, KV head); each wave
@@ -249,16 +257,22 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
 #pragma unroll
     for (int gb = 0; gb < 4; ++gb) cok[gb] = b0 + 16 * gb + r16 >= 0 && b0 + 16 * gb + r16 < n_cand;
     const int rows = n_q * group;
-    for (int chunk = wave; chunk < rows / 16; chunk += NW) {
-        // A operand: query row chunk*16 + r16 of (layer l, KV head g)
-        const int r = chunk * 16 + r16;
+    for (int chunk = wave; chunk < (rows + 15) / 16; chunk += NW) {
+        // A operand: query row chunk*16 + r16 of (layer l, KV head g); in a
+        // ragged last chunk the rows past the head's count are zero queries
+        // (read at the last row's address) and are never written
+        const int r = min(chunk * 16 + r16, rows - 1);
+        const bool a_ok = chunk * 16 + r16 < rows;
         const int64_t qrow = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
         f64x4_t st[4];
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
         float4 qa[NC];  // the chunk's query slices, all in flight before the products start
 #pragma unroll
-        for (int c = 0; c < NC; ++c) qa[c] = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
+        for (int c = 0; c < NC; ++c) {
+            const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
+            qa[c] = a_ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
         float4 bn[4];
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) bn[gb] = sm_idx[kg][16 * gb + r16];
@@ -285,6 +299,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rr = chunk * 16 + kg + 4 * i;
+            if (rr >= rows) continue;  // uniform over the 16 lanes that share this row
             const int64_t row = ((int64_t)l * n_q + rr / group) * n_q_heads + g * group + rr % group;
             float sv[4];
             float mx = -INFINITY;
@@ -512,12 +527,17 @@ hipError_t launch_logits(const SelectPlan &p, const float *q, const float *index
 template <int D>
 hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *index, float scale,
                            float *logits, float *tmax, double *tsum, hipStream_t stream) {
+    static_assert(kScoreVectorRows == 8, "vector kernels for 1 to 8 rows");
     switch (p.rows_per_head) {
         case 1: return launch_logits<D, 1>(p, q, index, scale, logits, tmax, tsum, stream);
         case 2: return launch_logits<D, 2>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 3: return launch_logits<D, 3>(p, q, index, scale, logits, tmax, tsum, stream);
         case 4: return launch_logits<D, 4>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 5: return launch_logits<D, 5>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 6: return launch_logits<D, 6>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 7: return launch_logits<D, 7>(p, q, index, scale, logits, tmax, tsum, stream);
         case 8: return launch_logits<D, 8>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 16: {
+        case 9: case 10: case 11: case 12: case 13: case 14: case 15: case 16: {
             dim3 grid(p.n_parts, p.n_kv_heads, p.n_layers);
             hipLaunchKernelGGL((score_logits_mfma16_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
                                p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
@@ -526,7 +546,7 @@ hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *ind
             return hipGetLastError();
         }
         default: {
-            if (p.rows_per_head % 16 != 0 || p.tiles_per_part != 1) return hipErrorInvalidValue;
+            if (p.tiles_per_part != 1) return hipErrorInvalidValue;
             dim3 grid(p.n_tiles, p.n_kv_heads, p.n_layers);
             hipLaunchKernelGGL((score_logits_rows_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
                                p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,

@@ -12,11 +12,19 @@ Acceptance rules (the tolerances are written here, once):
   * Attention: within 2e-2 absolute for bf16 K/V and 1e-4 for fp32 K/V,
     elementwise, on the same view.  FP8 K/V takes the low-precision bound
     (2e-2), against the oracle on the same codes decoded in fp64.
+  * Attention, regression bound: the kernels keep q and the softmax weights
+    at fp32 accuracy (hi + lo bf16 pairs on the matrix cores) and accumulate
+    in fp32, so their measured error is 1e-7 to 2e-6 on the output and about
+    1e-5 on the log-sum-exp.  Every case must also stay within 1e-4 of the
+    oracle (output and log-sum-exp, every K/V type), so that losing the lo
+    halves (about 1e-3 of error) or an fp32 accumulation step fails even
+    though it would pass the 2e-2 contract bound.
 """
 import numpy as np
 
 BAND = 1e-5
 ATOL = {"bf16": 2e-2, "f32": 1e-4, "fp8": 2e-2}
+REGRESSION_ATOL = 1e-4
 SCORE_RTOL = 1e-5
 
 
@@ -100,11 +108,16 @@ def check_scores(gpu_scores: np.ndarray, relevance: np.ndarray, n_sink: int, n_r
 
 
 def check_attention(out: np.ndarray, lse: np.ndarray, ref_out: np.ndarray, ref_lse: np.ndarray,
-                    kv_dtype: str):
+                    kv_dtype: str, regression: bool = True):
+    """Contract bound, then (unless regression=False, for inputs far outside the
+    workloads' value range) the regression bound."""
     atol = ATOL[kv_dtype]
     err = float(np.abs(out.astype(np.float64) - ref_out).max())
     lerr = float(np.abs(lse.astype(np.float64) - ref_lse).max())
     assert np.isfinite(out).all() and np.isfinite(lse).all()
     assert err <= atol, f"attention max abs error {err:.3g} > {atol}"
     assert lerr <= atol, f"lse max abs error {lerr:.3g} > {atol}"
+    if regression:
+        assert err <= REGRESSION_ATOL, f"attention max abs error {err:.3g} > regression bound {REGRESSION_ATOL}"
+        assert lerr <= REGRESSION_ATOL, f"lse max abs error {lerr:.3g} > regression bound {REGRESSION_ATOL}"
     return err, lerr

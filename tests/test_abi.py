@@ -57,7 +57,7 @@ def test_geometry_validation(L):
     z = ctypes.c_int32()
     assert _status(L.kvmem_plan_view(None, 100, 0, 4, 10**6, 10**6, None, None)) == "KVMEM_ERR_NULL"
     assert "geom" in K.kvmem_last_error()
-    for bad, st in [(dict(n_q_heads=30), "KVMEM_ERR_SHAPE"), (dict(n_kv_heads=3, n_q_heads=12), "KVMEM_ERR_UNSUPPORTED"),
+    for bad, st in [(dict(n_q_heads=30), "KVMEM_ERR_SHAPE"), (dict(n_kv_heads=65, n_q_heads=130), "KVMEM_ERR_UNSUPPORTED"),
                     (dict(head_dim=96), "KVMEM_ERR_UNSUPPORTED"), (dict(block_tokens=8), "KVMEM_ERR_UNSUPPORTED"),
                     (dict(kv_dtype=7), "KVMEM_ERR_DTYPE")]:
         rc = L.kvmem_plan_view(ctypes.byref(g1(**bad)), 100, 0, 4, 10**6, 10**6, ctypes.byref(z), None)
@@ -84,6 +84,20 @@ def test_plan_view_budget_cases():
     assert e.value.status == -5
     with pytest.raises(K.KvmemError):
         K.kvmem_plan_view(g, 100, 50, 50, 10**6, 10**6)  # no candidate left
+
+
+def test_any_gqa_width_is_accepted():
+    """Every G * n_q up to 4,096 rows per KV head and every KV head count up to 64
+    is a valid selection and attention shape (Eq. 10's head map g(h) is general)."""
+    for hkv, hq in [(8, 24), (8, 40), (6, 36), (4, 28), (3, 12), (5, 5), (7, 56), (64, 64)]:
+        for n_q in (1, 3, 4, 9):
+            g = K.Geom(hkv, hq, 128, 16, K.KVMEM_BF16)
+            assert K.kvmem_select_workspace_bytes(g, 1, n_q, 4096, 0, 64, K.KVMEM_REDUCE_MEAN_ALL) > 0
+            assert K.kvmem_select_workspace_bytes(g, 2, n_q, 4096, 1, 64, K.KVMEM_REDUCE_MAX_GROUP) > 0
+            assert K.kvmem_sparse_attn_workspace_bytes(g, n_q, hkv, 512) > 0
+    with pytest.raises(K.KvmemError) as e:
+        K.kvmem_select_workspace_bytes(K.Geom(8, 32, 128, 16, K.KVMEM_BF16), 1, 1025, 4096, 0, 64, 0)
+    assert e.value.status == -2 or "4096" in str(e.value)
 
 
 def test_workspace_queries():
@@ -133,8 +147,6 @@ def test_select_validation(L):
     assert _select(L, g, model=1000, ws_bytes=big) == "KVMEM_ERR_BUDGET"
     assert _select(L, g, n_recent=4096, ws_bytes=big) == "KVMEM_ERR_SHAPE"
     assert _select(L, g, mode=5, ws_bytes=big) == "KVMEM_ERR_SHAPE"
-    assert _select(L, g, n_q=3, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 12
-    assert _select(L, g, n_q=9, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 36
     assert _select(L, g, n_q=1028, ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"  # G*n_q = 4112 > 4096
     assert _select(L, g, n_blocks=(1 << 20) + 1024, n_recent=512, model=10**9, gpu=10**9,
                    ws_bytes=big) == "KVMEM_ERR_UNSUPPORTED"

@@ -53,16 +53,31 @@ def bf16_close(gpu_bits, ref64):
     return float((np.asarray(gpu_bits, np.uint16) != oracle.to_bf16_bits(ref64)).mean())
 
 
-@pytest.mark.parametrize("name,baked", [("tiny", "orig"), ("64k", "orig"), ("64k", "random")])
+# Workloads of the index-from-encoded-keys cases beyond the named ones: 64-token
+# blocks (the 4-layer workload's geometry) and fp32 keys at d = 128.
+ROPE_CFGS = {
+    "bt64": W.CONFIGS["64k"].replace(block_tokens=64, history_tokens=1024 * 64),
+    "f32_d128": W.small_config(n_kv_heads=4, n_q_heads=16, head_dim=128, block_tokens=32, kv_dtype="f32",
+                               history_tokens=600 * 32, recent_tokens=4 * 32, budget_tokens=64 * 32),
+}
+
+
+@pytest.mark.parametrize("name,baked", [("tiny", "orig"), ("64k", "orig"), ("64k", "random"), ("64k", "huge"),
+                                        ("bt64", "orig"), ("bt64", "random"), ("f32_d128", "orig"),
+                                        ("f32_d128", "random")])
 def test_index_from_encoded_keys(name, baked):
-    cfg = W.CONFIGS[name]
+    cfg = ROPE_CFGS[name] if name in ROPE_CFGS else W.CONFIGS[name]
     log(f"[case] index from encoded keys {name} positions={baked}")
     w = W.generate(cfg, cfg.seed, with_values=False)
     m = cfg.n_blocks
     if baked == "orig":
         p0, bp = np.arange(m, dtype=np.int64) * cfg.block_tokens, None
-    else:  # baked positions far beyond the window, e.g. after many delta moves
+    elif baked == "random":  # baked positions far beyond the window, e.g. after many delta moves
         p0 = np.random.default_rng(7).integers(0, 2 ** 40, m).astype(np.int64)
+        bp = p0
+    else:  # positions from 2^41 to 2^50 (both sides of the switch to per-token cos/sin at 2^42)
+        p0 = np.random.default_rng(7).integers(2 ** 41, 2 ** 50, m).astype(np.int64)
+        p0[::7] = 2 ** 42 - cfg.block_tokens - np.arange(p0[::7].size) % 3  # ends just below the switch
         bp = p0
     enc = encode_pool(w.k_pool[0], w.block_to_page, p0, BASE, cfg.kv_dtype == "bf16")
     ref = oracle.mean_k_rope(enc, w.block_to_page, BASE, block_pos=bp)
@@ -79,24 +94,31 @@ def test_index_from_encoded_keys(name, baked):
     assert np.abs(plain - ref).max() > 1e-2
 
 
-@pytest.mark.parametrize("d,bt", [(128, 16), (64, 32)])
-def test_index_from_encoded_fp8_keys(d, bt):
+@pytest.mark.parametrize("d,bt,explicit", [(128, 16, True), (64, 32, True), (128, 16, False), (64, 64, False),
+                                            (128, 64, True)])
+def test_index_from_encoded_fp8_keys(d, bt, explicit):
     """FP8 pools whose codes hold RoPE-encoded keys (encoded by the oracle in
-    fp64, then quantised like every FP8 pool)."""
+    fp64, then quantised like every FP8 pool), at explicit positions (the kernel
+    with the rounding correction) or at the original frame b * Bt below 2^26
+    (block_pos NULL: the kernel without it)."""
     cfg = W.CONFIGS["64k"].replace(kv_dtype="fp8", kv_scale=float(np.float32(8 / 448)), head_dim=d,
                                    block_tokens=bt, history_tokens=2048 * bt, n_kv_heads=4, n_q_heads=16)
-    log(f"[case] index from encoded FP8 keys d={d} Bt={bt}")
+    log(f"[case] index from encoded FP8 keys d={d} Bt={bt} explicit positions={explicit}")
     w = W.generate(cfg, 5, with_values=False)
     m = cfg.n_blocks
-    p0 = np.random.default_rng(8).integers(0, 2 ** 30, m).astype(np.int64)
+    if explicit:
+        p0 = np.random.default_rng(8).integers(0, 2 ** 30, m).astype(np.int64)
+    else:
+        p0 = np.arange(m, dtype=np.int64) * bt
     raw = oracle.decode_fp8(w.k_pool[0], cfg.kv_scale)
     pos = np.zeros(raw.shape[:3], np.int64)
     pos[w.block_to_page] = p0[:, None, None] + np.arange(bt)[None, None, :]
     codes = W.fp8_codes(oracle.rope(raw, pos, BASE).astype(np.float32), cfg.kv_scale)
-    ref = oracle.mean_k_rope(oracle.decode_fp8(codes, cfg.kv_scale), w.block_to_page, BASE, block_pos=p0)
+    ref = oracle.mean_k_rope(oracle.decode_fp8(codes, cfg.kv_scale), w.block_to_page, BASE,
+                             block_pos=p0 if explicit else None)
     st = LayerState(cfg, codes, None, w.block_to_page)
     K.kvmem_build_index_rope(st.geom, st.k_pool, st.block_to_page, 0, m, st.index, BASE,
-                             torch.from_numpy(p0).cuda())
+                             torch.from_numpy(p0).cuda() if explicit else None)
     torch.cuda.synchronize()
     got = st.index_rows()
     err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
