@@ -306,6 +306,26 @@ kvmem_status kvmem_select(const kvmem_geom *geom, int32_t n_layers, const float 
                           int32_t *view_pages, float *scores, int32_t *n_view_out,
                           void *workspace, size_t workspace_bytes, void *stream);
 
+/* kvmem_select without a caller workspace, for callers that cannot allocate
+ * device memory around the call (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Arguments, results and errors are
+ * those of kvmem_select; the scratch space is a device array inside the library
+ * (one per GPU, KVMEM_SELECT_NOALLOC_MAX_BYTES, held until the process ends),
+ * so the call never allocates or frees memory.  A selection whose workspace
+ * (kvmem_select_workspace_bytes) exceeds that size returns KVMEM_ERR_WORKSPACE
+ * -- 16 MiB covers a decode step's selection over 2^20 candidates at 32 query
+ * rows, not a recall point's thousands of rows.  `stream` must run on the
+ * current device (KVMEM_ERR_UNSUPPORTED otherwise).  Every call on one GPU
+ * uses the same scratch: calls that overlap in time on one GPU (other streams,
+ * other threads) race and must be serialised by the caller. */
+#define KVMEM_SELECT_NOALLOC_MAX_BYTES (16u << 20)
+kvmem_status kvmem_select_noalloc(const kvmem_geom *geom, int32_t n_layers, const float *q,
+                                  int32_t n_q_tokens, const float *index, int32_t n_blocks,
+                                  int32_t n_sink_blocks, int32_t n_recent_blocks,
+                                  int64_t model_ctx_tokens, int64_t gpu_kv_tokens, int32_t mode,
+                                  float scale, const int32_t *block_to_page, int32_t *view_blocks,
+                                  int32_t *view_pages, float *scores, int32_t *n_view_out, void *stream);
+
 /* Bytes of workspace kvmem_sparse_attn needs for these sizes (0 on invalid input). */
 size_t kvmem_sparse_attn_workspace_bytes(const kvmem_geom *geom, int32_t n_q_tokens,
                                          int32_t n_sel, int32_t n_view);

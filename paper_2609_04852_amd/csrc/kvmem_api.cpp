@@ -7,9 +7,16 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 
 #include "kvmem_internal.h"
+
+// Scratch of kvmem_select_noalloc: a file-scope device array, one copy per GPU
+// that loads this library, held until the process ends.  Host code never uses
+// its name as an address: each device's address is looked up once with
+// hipGetSymbolAddress (with that device current) and kept in g_scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[KVMEM_SELECT_NOALLOC_MAX_BYTES];
 
 namespace {
 
@@ -162,6 +169,49 @@ kvmem_status make_attn_plan(const kvmem_geom *g, int32_t n_q, int32_t n_sel, int
 kvmem_status hip_status(hipError_t e, const char *what) {
     if (e == hipSuccess) return ok();
     return fail(KVMEM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Arguments of kvmem_select other than the workspace: checked on the host.
+kvmem_status check_select_args(const kvmem_geom *geom, const float *q, const float *index,
+                               const int32_t *block_to_page, const int32_t *view_blocks,
+                               const int32_t *view_pages, const float *scores) {
+    if (!q || !index || !block_to_page || !view_blocks || !view_pages)
+        return fail(KVMEM_ERR_NULL, "q, index, block_to_page, view_blocks and view_pages must be non-NULL");
+    if (!aligned16(q) || !aligned16(index) || !aligned16(block_to_page) || !aligned16(view_blocks) ||
+        !aligned16(view_pages) || (scores && !aligned16(scores)))
+        return fail(KVMEM_ERR_ALIGN, "device pointers must be 16-byte aligned");
+    return KVMEM_OK;
+}
+
+// Device address of `scratch` on the device that runs `stream` (which must be
+// the current device), looked up on the first call on that device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+kvmem_status scratch_for(void *stream, char **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    if (stream) {
+        int sdev = -1;
+        if ((e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev)) != hipSuccess)
+            return hip_status(e, "hipStreamGetDevice");
+        if (sdev != dev)
+            return fail(KVMEM_ERR_UNSUPPORTED, "the stream runs on device %d but device %d is current", sdev, dev);
+    }
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(KVMEM_ERR_UNSUPPORTED, "device %d: at most %d devices are supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(KVMEM_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL on device %d", dev);
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = static_cast<char *>(g_scratch_ptr[dev]);
+    return KVMEM_OK;
 }
 
 }  // namespace
@@ -383,19 +433,42 @@ kvmem_status kvmem_select(const kvmem_geom *geom, int32_t n_layers, const float 
     kvmem_status st = make_select_plan(geom, n_layers, n_q_tokens, n_blocks, n_sink_blocks,
                                        n_recent_blocks, model_ctx_tokens, gpu_kv_tokens, mode, p);
     if (st != KVMEM_OK) return st;
-    if (!q || !index || !block_to_page || !view_blocks || !view_pages)
-        return fail(KVMEM_ERR_NULL, "q, index, block_to_page, view_blocks and view_pages must be non-NULL");
+    if ((st = check_select_args(geom, q, index, block_to_page, view_blocks, view_pages, scores)) != KVMEM_OK)
+        return st;
     if (!workspace || workspace_bytes < p.total)
         return fail(KVMEM_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required",
                     workspace_bytes, p.total);
-    if (!aligned16(q) || !aligned16(index) || !aligned16(block_to_page) || !aligned16(view_blocks) ||
-        !aligned16(view_pages) || (scores && !aligned16(scores)) || !aligned16(workspace))
-        return fail(KVMEM_ERR_ALIGN, "device pointers must be 16-byte aligned");
+    if (!aligned16(workspace)) return fail(KVMEM_ERR_ALIGN, "device pointers must be 16-byte aligned");
     if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)geom->head_dim);
     if (n_view_out) *n_view_out = p.n_view;
     return hip_status(kvmem::launch_select(p, q, index, scale, block_to_page, view_blocks, view_pages,
                                            scores, static_cast<char *>(workspace),
                                            static_cast<hipStream_t>(stream)),
+                      "select launch");
+}
+
+kvmem_status kvmem_select_noalloc(const kvmem_geom *geom, int32_t n_layers, const float *q,
+                                  int32_t n_q_tokens, const float *index, int32_t n_blocks,
+                                  int32_t n_sink_blocks, int32_t n_recent_blocks,
+                                  int64_t model_ctx_tokens, int64_t gpu_kv_tokens, int32_t mode,
+                                  float scale, const int32_t *block_to_page, int32_t *view_blocks,
+                                  int32_t *view_pages, float *scores, int32_t *n_view_out, void *stream) {
+    kvmem::SelectPlan p;
+    kvmem_status st = make_select_plan(geom, n_layers, n_q_tokens, n_blocks, n_sink_blocks,
+                                       n_recent_blocks, model_ctx_tokens, gpu_kv_tokens, mode, p);
+    if (st != KVMEM_OK) return st;
+    if ((st = check_select_args(geom, q, index, block_to_page, view_blocks, view_pages, scores)) != KVMEM_OK)
+        return st;
+    if (p.total > (size_t)KVMEM_SELECT_NOALLOC_MAX_BYTES)
+        return fail(KVMEM_ERR_WORKSPACE,
+                    "this selection needs %zu bytes of scratch; kvmem_select_noalloc has %zu "
+                    "(use kvmem_select with a workspace)", p.total, (size_t)KVMEM_SELECT_NOALLOC_MAX_BYTES);
+    char *ws = nullptr;
+    if ((st = scratch_for(stream, &ws)) != KVMEM_OK) return st;
+    if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)geom->head_dim);
+    if (n_view_out) *n_view_out = p.n_view;
+    return hip_status(kvmem::launch_select(p, q, index, scale, block_to_page, view_blocks, view_pages,
+                                           scores, ws, static_cast<hipStream_t>(stream)),
                       "select launch");
 }
 

@@ -85,6 +85,8 @@ def lib() -> ctypes.CDLL:
     L.kvmem_select_workspace_bytes.restype = sz
     L.kvmem_select.argtypes = [G, i32, P, i32, P, i32, i32, i32, i64, i64, i32, f32, P, P, P, P,
                                pi32, P, sz, P]
+    L.kvmem_select_noalloc.argtypes = [G, i32, P, i32, P, i32, i32, i32, i64, i64, i32, f32, P, P, P, P,
+                                       pi32, P]
     L.kvmem_sparse_attn_workspace_bytes.argtypes = [G, i32, i32, i32]
     L.kvmem_sparse_attn_workspace_bytes.restype = sz
     L.kvmem_sparse_attn.argtypes = [G, P, i32, P, P, i64, P, i32, i32, i32, f32, P, P, P, sz, P]
@@ -97,7 +99,7 @@ def lib() -> ctypes.CDLL:
     L.kvmem_working_set_workspace_bytes.argtypes = [i32, i32]
     L.kvmem_working_set_workspace_bytes.restype = sz
     L.kvmem_working_set_update.argtypes = [G, dbl, W, i32, P, i32, i64, i32, P, P, P, i64, P, P, P, P, P, sz, P]
-    for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_sparse_attn",
+    for name in ("kvmem_build_index", "kvmem_plan_view", "kvmem_select", "kvmem_select_noalloc", "kvmem_sparse_attn",
                  "kvmem_build_index_rope", "kvmem_materialize", "kvmem_rerope", "kvmem_working_set_reset",
                  "kvmem_working_set_update"):
         getattr(L, name).restype = ctypes.c_int
@@ -233,6 +235,43 @@ def kvmem_select(geom: Geom, q: torch.Tensor, index: torch.Tensor, n_blocks: int
                               _ptr(block_to_page), _ptr(view_blocks), _ptr(view_pages), _ptr(scores),
                               ctypes.byref(out_n), _ptr(workspace), workspace.numel(),
                               _stream(stream)))
+    return out_n.value
+
+
+SELECT_NOALLOC_MAX_BYTES = 16 << 20  # KVMEM_SELECT_NOALLOC_MAX_BYTES
+
+
+def kvmem_select_noalloc(geom: Geom, q: torch.Tensor, index: torch.Tensor, n_blocks: int, n_sink: int,
+                         n_recent: int, model_ctx_tokens: int, gpu_kv_tokens: int, mode: int, scale: float,
+                         block_to_page: torch.Tensor, view_blocks: torch.Tensor, view_pages: torch.Tensor,
+                         scores: torch.Tensor | None = None, stream=None) -> int:
+    """kvmem_select with the library's own device scratch instead of a workspace
+    (no allocation around the call).  Returns n_view."""
+    _need(q, torch.float32, "q")
+    _need(index, torch.float32, "index")
+    _need(block_to_page, torch.int32, "block_to_page")
+    _need(view_blocks, torch.int32, "view_blocks")
+    _need(view_pages, torch.int32, "view_pages")
+    if q.dim() != 4 or tuple(q.shape[2:]) != (geom.n_q_heads, geom.head_dim):
+        raise ValueError("q must be [L][n_q][Hq][d]")
+    n_layers, n_q = q.shape[0], q.shape[1]
+    if index.numel() * 4 < n_layers * kvmem_index_bytes(geom, n_blocks):
+        raise ValueError("index is smaller than n_layers tiled layers of n_blocks blocks")
+    if block_to_page.numel() != n_blocks:
+        raise ValueError("block_to_page must have one entry per block")
+    k_eff, n_view = kvmem_plan_view(geom, n_blocks, n_sink, n_recent, model_ctx_tokens, gpu_kv_tokens)
+    n_sel = 1 if mode == KVMEM_REDUCE_MEAN_ALL else n_layers * geom.n_kv_heads
+    if view_blocks.numel() < n_sel * n_view or view_pages.numel() < n_sel * n_view:
+        raise ValueError("view tables are smaller than n_sel * n_view")
+    if scores is not None:
+        _need(scores, torch.float32, "scores")
+        if scores.numel() < n_sel * n_blocks:
+            raise ValueError("scores is smaller than n_sel * n_blocks")
+    out_n = ctypes.c_int32()
+    _check(lib().kvmem_select_noalloc(ctypes.byref(geom.c()), n_layers, _ptr(q), n_q, _ptr(index), n_blocks,
+                                      n_sink, n_recent, model_ctx_tokens, gpu_kv_tokens, mode, scale,
+                                      _ptr(block_to_page), _ptr(view_blocks), _ptr(view_pages), _ptr(scores),
+                                      ctypes.byref(out_n), _stream(stream)))
     return out_n.value
 
 
