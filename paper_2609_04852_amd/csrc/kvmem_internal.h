@@ -32,8 +32,10 @@ __host__ __device__ inline int64_t index_layer_floats(int64_t n_blocks, int n_kv
 // kernel (rows past the head's count padded with zero queries), more by
 // 16-row chunks.
 constexpr int kScoreTilesPerGroup = 4;
-constexpr int kMfma16Tiles = 1;
 constexpr int kScoreVectorRows = 8;
+// The 16-row kernel's waves are persistent: about kMfma16Waves of them over
+// all (layer, KV head) pairs, four per workgroup, each leaving one partial.
+constexpr int kMfma16Waves = 2048;
 // More than 16 query rows per KV head (a recall point's prefill query): one
 // workgroup per index tile runs every row of its (layer, KV head) in chunks of
 // 16 on the matrix cores; the block relevance then sums the rows in
@@ -56,7 +58,7 @@ struct SelectPlan {
     int n_rows;   // n_layers * n_q * n_q_heads
     int tile_lo;     // first index tile holding a candidate
     int n_tiles;     // index tiles holding candidates
-    int tiles_per_part;  // index tiles per logit workgroup
+    int tiles_per_part;  // index tiles per logit workgroup (0: the persistent 16-row kernel)
     int n_parts;     // logit workgroups along the candidates = partial stats per row
     int n_rsplit;    // row partitions of the block-relevance sum (1: one pass)
     int cand_stride; // row stride of logits and score rows (n_cand rounded up to 64)
@@ -82,9 +84,19 @@ inline void plan_select_layout(SelectPlan &p) {
     p.n_rows = p.n_layers * p.n_q * p.n_q_heads;
     p.tile_lo = p.n_sink / kIndexTile;
     p.n_tiles = (int)index_tiles(p.n_blocks - p.n_recent) - p.tile_lo;
-    p.tiles_per_part = p.rows_per_head > 16 ? 1 : p.rows_per_head > kScoreVectorRows ? kMfma16Tiles
-                                                                                   : kScoreTilesPerGroup;
-    p.n_parts = (p.n_tiles + p.tiles_per_part - 1) / p.tiles_per_part;
+    if (p.rows_per_head > 16) {
+        p.tiles_per_part = 1;
+        p.n_parts = p.n_tiles;
+    } else if (p.rows_per_head > kScoreVectorRows) {  // persistent waves: n_parts = 4 x workgroups
+        const int heads = p.n_layers * p.n_kv_heads;
+        int wg = (kMfma16Waves / 4 + heads - 1) / heads;
+        if (wg > p.n_tiles) wg = p.n_tiles;  // at least one 16-block group per wave
+        p.tiles_per_part = 0;
+        p.n_parts = 4 * (wg > 0 ? wg : 1);
+    } else {
+        p.tiles_per_part = kScoreTilesPerGroup;
+        p.n_parts = (p.n_tiles + p.tiles_per_part - 1) / p.tiles_per_part;
+    }
     {
         const int nr = p.mode == 0 ? p.n_rows : p.n_q * p.group;  // logit rows behind one relevance value
         int parts = nr / kReduceRowsPerPart;

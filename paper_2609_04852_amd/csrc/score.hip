@@ -103,17 +103,18 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
 // logit is the fp32 rounding of the exact dot product (the vector kernel's
 // fp32 accumulation, and the fp32 matrix cores even more, lose a few ulps at
 // the logit magnitudes of clustered keys, which the selection's 1e-5 band
-// cannot afford).  One workgroup per (kMfma16Tiles index tiles, KV head):
-// wave w takes 16-block group w of each of the tiles, and issues the loads of
-// all of them before its first MFMA (a wave with a whole tile would load all
-// 64 blocks, then run 128 MFMAs in dependent chains with nothing else in
-// flight; with a group per tile, more waves fit a SIMD and the matrix unit
-// works on whichever wave's data has arrived).  For one group, S^T = index
-// Q^T: lane l loads, for each 16-dim slice c, the 4 dims 16c + 4kg .. of block
-// l%16 (kg = l/16) as one float4 from the tiled index and feeds them to 4
-// MFMAs whose contraction slot kg stands for those dims; Q^T is the matching B
-// operand, kept in registers.  Lane l receives the logits of row l%16 for
-// blocks kg, kg+4, kg+8, kg+12 of the group.
+// cannot afford).  For one 16-block group of a tile, S^T = index Q^T: lane l
+// loads, for each 16-dim slice c, the 4 dims 16c + 4kg .. of block l%16 (kg =
+// l/16) as one float4 from the tiled index and feeds them to 4 MFMAs whose
+// contraction slot kg stands for those dims; Q^T is the matching B operand,
+// kept in registers.  Lane l receives the logits of row l%16 for blocks kg,
+// kg+4, kg+8, kg+12 of the group.
+// The waves are persistent and pipelined: wave w of workgroup j takes the
+// head's groups 4j + w, 4j + w + n_parts, ... and loads the next group while
+// the current group's 32 MFMAs run, so the index stream and the matrix cores
+// overlap.  Each wave keeps an online (max, sum of exp) per row over its
+// groups -- the sum rescaled in fp64 when the maximum grows -- and leaves one
+// partial per row: n_parts = workgroups x 4 partials per row.
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
@@ -122,13 +123,11 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
     int n_tiles, int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
     double *__restrict__ tsum) {
-    constexpr int RH = 16, NW = kScoreThreads / kWave, NC = D / 16, NT = kMfma16Tiles;
-    static_assert(NW * 16 == kIndexTile, "one 16-block group per wave");
-    __shared__ float sm_m[NW][RH];
-    __shared__ double sm_s[NW][RH];
+    constexpr int NW = kScoreThreads / kWave, NC = D / 16;
+    static_assert(NW * 16 == kIndexTile, "four 16-block groups per tile");
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r16 = lane % 16, kg = lane / 16;
-    const int g = blockIdx.y, l = blockIdx.z, gb = wave;
+    const int g = blockIdx.y, l = blockIdx.z;
     // the head's rows (9 to 16): lanes of rows past them hold zero queries
     // (a copy of the last row's address, never written)
     const int rows = group * n_q;
@@ -136,19 +135,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     const int rr = row_ok ? r16 : rows - 1;
     const int64_t qrow = ((int64_t)l * n_q + rr / group) * n_q_heads + g * group + rr % group;
     const int64_t tiles_per_layer = index_tiles(n_blocks);
+    const int part = blockIdx.x * NW + wave;  // this wave's partial; n_parts waves per (layer, head)
+    const int n_groups = n_tiles * NW;
 
-    // the group's loads of every tile of the workgroup first (a tile past the
-    // candidates reads the last one again), then the query operand
-    float4 x[NT][NC];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int tile = tile_lo + min(blockIdx.x * NT + t, n_tiles - 1);
+    auto load = [&](int gi, float4 (&x)[NC]) {
+        const int tile = tile_lo + gi / NW, gb = gi % NW;
         const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
-                                       (int64_t)(D / 4) * (kIndexTile * 4);
+                                       (int64_t)(D / 4) * (kIndexTile * 4) + (16 * gb + r16) * 4;
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
-            x[t][c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4) + (16 * gb + r16) * 4);
-    }
+        for (int c = 0; c < NC; ++c) x[c] = *reinterpret_cast<const float4 *>(src + (4 * c + kg) * (kIndexTile * 4));
+    };
+    float4 xa[NC], xb[NC];
+    int gi = part;
+    if (gi < n_groups) load(gi, xa);
     // B operand: q[row r16][16c + 4kg + e] (the scale is applied to the sum)
     float qv[NC][4];
 #pragma unroll
@@ -157,65 +156,61 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
         qv[c][0] = row_ok ? v.x : 0.f; qv[c][1] = row_ok ? v.y : 0.f;
         qv[c][2] = row_ok ? v.z : 0.f; qv[c][3] = row_ok ? v.w : 0.f;
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep every load in flight together
-    float s[NT][4];  // tile t, row r16, block 16 * gb + kg + 4i
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
+    float mrun = -INFINITY;  // row r16 (the same in its 4 kg lanes)
+    double srun = 0.0;
+    auto compute = [&](int gj, const float4 (&x)[NC]) {
         f64x4_t st = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
+        for (int c = 0; c < NC; ++c) {
+            const float xv[4] = {x[c].x, x[c].y, x[c].z, x[c].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                st = __builtin_amdgcn_mfma_f64_16x16x4f64((double)x[t][c][e], (double)qv[c][e], st, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s[t][i] = (float)(st[i] * (double)scale);
-    }
-    // logits (4 blocks per lane and tile, 4 apart) and per-row stats
-    auto valid = [&](int t, int i, int64_t &c) {
-        c = (int64_t)(tile_lo + blockIdx.x * NT + t) * kIndexTile + 16 * gb + kg + 4 * i - n_sink;
-        return blockIdx.x * NT + t < n_tiles && c >= 0 && c < n_cand;
-    };
-    float mx = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
+                st = __builtin_amdgcn_mfma_f64_16x16x4f64((double)xv[e], (double)qv[c][e], st, 0, 0, 0);
+        }
+        // logits of blocks kg + 4i of the group, and the online row stats
+        const int64_t c0 = (int64_t)(tile_lo + gj / NW) * kIndexTile + 16 * (gj % NW) + kg - n_sink;
+        float s[4];
+        bool ok[4];
+        float gm = -INFINITY;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            int64_t c;
-            const bool ok = valid(t, i, c);
-            if (ok && row_ok) logits[qrow * cand_stride + c] = s[t][i];
-            mx = fmaxf(mx, ok ? s[t][i] : -INFINITY);
+            s[i] = (float)(st[i] * (double)scale);
+            const int64_t c = c0 + 4 * i;
+            ok[i] = c >= 0 && c < n_cand;
+            if (ok[i] && row_ok) logits[qrow * cand_stride + c] = s[i];
+            gm = fmaxf(gm, ok[i] ? s[i] : -INFINITY);
         }
-    mx = fmaxf(mx, shfl_xor_f(mx, 16));
-    mx = fmaxf(mx, shfl_xor_f(mx, 32));
-    double e = 0.0;
-    if (mx != -INFINITY) {
+        gm = fmaxf(gm, shfl_xor_f(gm, 16));
+        gm = fmaxf(gm, shfl_xor_f(gm, 32));
+        if (gm > mrun) {
+            srun = mrun == -INFINITY ? 0.0 : srun * exp((double)mrun - (double)gm);
+            mrun = gm;
+        }
+        double e = 0.0;
+        if (mrun != -INFINITY) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                int64_t c;
-                if (valid(t, i, c)) e += (double)expf(s[t][i] - mx);
-            }
+            for (int i = 0; i < 4; ++i)
+                if (ok[i]) e += (double)expf(s[i] - mrun);
+        }
+        e += __shfl_xor(e, 16, kWave);
+        e += __shfl_xor(e, 32, kWave);
+        srun += e;
+    };
+    // two register buffers: the next group's loads are in flight during the
+    // current group's products
+    while (gi < n_groups) {
+        const int g1 = gi + n_parts;
+        if (g1 < n_groups) load(g1, xb);
+        compute(gi, xa);
+        if (g1 >= n_groups) break;
+        const int g2 = g1 + n_parts;
+        if (g2 < n_groups) load(g2, xa);
+        compute(g1, xb);
+        gi = g2;
     }
-    e += __shfl_xor(e, 16, kWave);
-    e += __shfl_xor(e, 32, kWave);
-    if (kg == 0) {
-        sm_m[wave][r16] = mx;
-        sm_s[wave][r16] = e;
-    }
-    __syncthreads();
-    if ((int)threadIdx.x < rows) {
-        const int r = threadIdx.x;
-        const int64_t qr = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
-        float m = sm_m[0][r];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) m = fmaxf(m, sm_m[w][r]);
-        double sum = 0.0;
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-            if (sm_m[w][r] != -INFINITY) sum += sm_s[w][r] * exp((double)sm_m[w][r] - (double)m);
-        tmax[qr * n_parts + blockIdx.x] = m;
-        tsum[qr * n_parts + blockIdx.x] = sum;
+    if (kg == 0 && row_ok) {
+        tmax[qrow * n_parts + part] = mrun;
+        tsum[qrow * n_parts + part] = srun;
     }
 }
 
@@ -538,7 +533,7 @@ hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *ind
         case 7: return launch_logits<D, 7>(p, q, index, scale, logits, tmax, tsum, stream);
         case 8: return launch_logits<D, 8>(p, q, index, scale, logits, tmax, tsum, stream);
         case 9: case 10: case 11: case 12: case 13: case 14: case 15: case 16: {
-            dim3 grid(p.n_parts, p.n_kv_heads, p.n_layers);
+            dim3 grid(p.n_parts / 4, p.n_kv_heads, p.n_layers);
             hipLaunchKernelGGL((score_logits_mfma16_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
                                p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
                                (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
