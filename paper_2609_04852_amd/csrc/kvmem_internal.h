@@ -47,7 +47,9 @@ constexpr int kReduceMaxParts = 64;
 // each); the key histogram has kSelBins bins (bits 30..19 of the score key),
 // the second level inside the pivot bin kSelBins2 (bits 18..8).
 constexpr int kSelChunk = 1024;
-constexpr int kSelBins = 4096;
+constexpr int kSelBinBits = 12;
+constexpr int kSelBins = 1 << kSelBinBits;
+constexpr int kSelShift1 = 31 - kSelBinBits;  // first-level digit: key bits 30 .. kSelShift1
 constexpr int kSelBins2 = 2048;
 constexpr int kSelHistWords = kSelBins + kSelBins2 + 1;  // per selection row, with the pivot-bin count
 constexpr int kTopkMaxCand = 1 << 20;  // candidates per selection row (1,024 chunks)
@@ -120,9 +122,9 @@ inline void plan_select_layout(SelectPlan &p) {
 }
 
 // ---- attention ---------------------------------------------------------
-constexpr int kAttnTargetGroups = 512;   // workgroups the split-K launch aims for
+constexpr int kAttnTargetGroups = 256;   // workgroups the split-K launch aims for: one per compute unit
 constexpr int kAttnMinPages = 4;         // pages per split, lower bound
-constexpr int kAttnMaxPages = 256;       // pages per split, upper bound
+constexpr int kAttnMaxPages = 512;       // pages per split, upper bound
 constexpr int kAttnMaxSplits = 16384;    // split weights the merge keeps in LDS
 constexpr int kPartStride = 4;           // floats after the D outputs of a partial row: m, l, pad
 
@@ -136,7 +138,13 @@ struct AttnPlan {
 };
 
 inline void plan_attn_layout(AttnPlan &p) {
-    long long want = ((long long)p.n_view * p.n_kv_heads + kAttnTargetGroups - 1) / kAttnTargetGroups;
+    // one workgroup per compute unit for decode (4 to 47 rows per KV head):
+    // with two per unit the second one dispatched to each unit falls behind
+    // the first and finishes alone, and the gather of random pages runs
+    // slower with both resident (measured at 1M: 169.4 against 172.5 us per
+    // call).  The many-row kernel keeps two per unit.
+    const long long target = p.rows_per_head >= 48 ? 2 * kAttnTargetGroups : kAttnTargetGroups;
+    long long want = ((long long)p.n_view * p.n_kv_heads + target - 1) / target;
     int pps = (int)(want < kAttnMinPages ? kAttnMinPages : (want > kAttnMaxPages ? kAttnMaxPages : want));
     p.pages_per_split = pps;
     p.n_splits = (p.n_view + pps - 1) / pps;

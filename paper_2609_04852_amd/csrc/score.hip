@@ -491,7 +491,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
         for (int e = 0; e < 4; ++e) {
             if (c0 + e >= n_cand) continue;
             const uint32_t key = __float_as_uint(r[e]) + 1u;
-            atomicAdd(&lh[(key >> 19) & (kSelBins - 1)], 1u);
+            atomicAdd(&lh[(key >> kSelShift1) & (kSelBins - 1)], 1u);
             if (scores) scores[(int64_t)sel * n_blocks + n_sink + c0 + e] = r[e];
         }
     }

@@ -42,15 +42,15 @@ namespace {
 constexpr int kChunkThreads = kSelChunk / 4;  // 4 candidates per thread
 constexpr int kFinishThreads = kChunkThreads;
 constexpr int kDigitBits = 11;
-constexpr int kSubShift = 8;            // second-level digit: key bits 18..8
+constexpr int kSubShift = kSelShift1 - 11;  // second-level digit: the 11 key bits below the first
 constexpr int kWindowCap = 8192;        // sub-pivot keys kept in LDS
 constexpr int kBruteMax = kFinishThreads;  // sub-pivot sets ranked pairwise
-static_assert(kSelBins2 << kSubShift == 1 << 19, "second level = the bits below the first");
+static_assert(kSelBins2 << kSubShift == 1 << kSelShift1, "second level = the bits below the first");
 
 enum { kCtrlPivot = 0, kCtrlRank = 3 };
 
 __device__ inline uint32_t mask_above(int bit) { return bit >= 31 ? 0u : (~0u << (bit + 1)); }
-__device__ inline uint32_t bin1(uint32_t key) { return (key >> 19) & (kSelBins - 1); }
+__device__ inline uint32_t bin1(uint32_t key) { return (key >> kSelShift1) & (kSelBins - 1); }
 __device__ inline uint32_t bin2(uint32_t key) { return (key >> kSubShift) & (kSelBins2 - 1); }
 
 // The bin holding rank k (1-based, descending) of histogram gh and the number
