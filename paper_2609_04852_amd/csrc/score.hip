@@ -215,8 +215,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
 }
 
 // More than 16 query rows per KV head (a recall point: the prefill's query
-// tokens x the group's heads; a ragged last 16-row chunk is padded with zero
-// queries that are never written).  The scoring is then a dense contraction,
+// tokens x the group's heads; a ragged last 16-row chunk repeats its last row,
+// whose copies are never written).  The scoring is then a dense contraction,
 // S = Q index^T, run on the fp64 matrix cores for the same reason as above.
 // One workgroup per (index tile, KV head, layer): the tile's 64 x D floats are
 // staged in LDS once and serve every row of that (layer, KV head); each wave
@@ -254,20 +254,16 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
     const int rows = n_q * group;
     for (int chunk = wave; chunk < (rows + 15) / 16; chunk += NW) {
         // A operand: query row chunk*16 + r16 of (layer l, KV head g); in a
-        // ragged last chunk the rows past the head's count are zero queries
-        // (read at the last row's address) and are never written
+        // ragged last chunk the rows past the head's count repeat the last
+        // row and their results are never written
         const int r = min(chunk * 16 + r16, rows - 1);
-        const bool a_ok = chunk * 16 + r16 < rows;
         const int64_t qrow = ((int64_t)l * n_q + r / group) * n_q_heads + g * group + r % group;
         f64x4_t st[4];
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) st[gb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
         float4 qa[NC];  // the chunk's query slices, all in flight before the products start
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const float4 v = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
-            qa[c] = a_ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        for (int c = 0; c < NC; ++c) qa[c] = *reinterpret_cast<const float4 *>(q + qrow * D + 16 * c + 4 * kg);
         float4 bn[4];
 #pragma unroll
         for (int gb = 0; gb < 4; ++gb) bn[gb] = sm_idx[kg][16 * gb + r16];
@@ -293,8 +289,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
         // lane: rows kg + 4i of the chunk, blocks 16gb + r16
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int rr = chunk * 16 + kg + 4 * i;
-            if (rr >= rows) continue;  // uniform over the 16 lanes that share this row
+            const int rr0 = chunk * 16 + kg + 4 * i;
+            const bool rok = rr0 < rows;  // the same in the 16 lanes that share this row
+            const int rr = rok ? rr0 : rows - 1;
             const int64_t row = ((int64_t)l * n_q + rr / group) * n_q_heads + g * group + rr % group;
             float sv[4];
             float mx = -INFINITY;
@@ -302,7 +299,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
             for (int gb = 0; gb < 4; ++gb) {
                 sv[gb] = (float)(st[gb][i] * (double)scale);
                 if (cok[gb]) {
-                    logits[row * cand_stride + b0 + 16 * gb + r16] = sv[gb];
+                    if (rok) logits[row * cand_stride + b0 + 16 * gb + r16] = sv[gb];
                     mx = fmaxf(mx, sv[gb]);
                 }
             }
@@ -316,7 +313,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_rows_kernel(
             }
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) e += __shfl_xor(e, o, kWave);
-            if (r16 == 0) {
+            if (r16 == 0 && rok) {
                 tmax[row * n_parts + blockIdx.x] = mx;
                 tsum[row * n_parts + blockIdx.x] = e;
             }
