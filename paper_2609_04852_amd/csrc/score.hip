@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
         }
     }
     __syncthreads();
-    uint32_t *gh = hist + (int64_t)sel * kSelBins;
+    uint32_t *gh = hist + ((int64_t)(blockIdx.x % kHistCopies) * gridDim.y + sel) * kSelBins;
     for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads)
         if (lh[i]) atomicAdd(&gh[i], lh[i]);
 }

@@ -55,16 +55,25 @@ __device__ inline uint32_t bin2(uint32_t key) { return (key >> kSubShift) & (kSe
 
 // The bin holding rank k (1-based, descending) of histogram gh and the number
 // of items in the bins above it (all threads of the workgroup get the values).
-template <int NT, int NBINS>
+// gh may hold COPIES copies of the histogram, copy_stride words apart, whose
+// counts add up.
+template <int NT, int NBINS, int COPIES = 1>
 __device__ void find_pivot(const uint32_t *__restrict__ gh, uint32_t k, uint32_t *scratch,
-                           uint32_t *s_out, uint32_t *pivot, uint32_t *above) {
+                           uint32_t *s_out, uint32_t *pivot, uint32_t *above, int64_t copy_stride = 0) {
     constexpr int PER = NBINS / NT;  // bins per thread, descending
     static_assert(PER * NT == NBINS, "bins divide evenly");
     uint32_t cnt[PER];
     uint32_t mine = 0u;
+    uint32_t part[COPIES][PER];
+#pragma unroll
+    for (int c = 0; c < COPIES; ++c)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) part[c][i] = gh[c * copy_stride + NBINS - 1 - (threadIdx.x * PER + i)];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        cnt[i] = gh[NBINS - 1 - (threadIdx.x * PER + i)];
+        cnt[i] = 0u;
+#pragma unroll
+        for (int c = 0; c < COPIES; ++c) cnt[i] += part[c][i];
         mine += cnt[i];
     }
     uint32_t total;
@@ -99,10 +108,12 @@ __device__ inline void load_chunk_keys(const float *R, int chunk, int n_cand, ui
 // Pointers into the histogram area of the workspace (n_sel rows).
 struct SelHist {
     uint32_t *h1, *h2, *count;
+    int64_t h1_stride;  // words between the copies of the first-level histogram
     __device__ SelHist(uint32_t *hist, int sel, int n_sel)
         : h1(hist + (int64_t)sel * kSelBins),
-          h2(hist + (int64_t)n_sel * kSelBins + (int64_t)sel * kSelBins2),
-          count(hist + (int64_t)n_sel * (kSelBins + kSelBins2) + sel) {}
+          h2(hist + (int64_t)kHistCopies * n_sel * kSelBins + (int64_t)sel * kSelBins2),
+          count(hist + (int64_t)n_sel * (kHistCopies * kSelBins + kSelBins2) + sel),
+          h1_stride((int64_t)n_sel * kSelBins) {}
 };
 
 __global__ __launch_bounds__(kChunkThreads) void sel_refine_kernel(
@@ -121,7 +132,8 @@ __global__ __launch_bounds__(kChunkThreads) void sel_refine_kernel(
     int c0;
     load_chunk_keys(r32 + (int64_t)sel * r_stride, chunk, n_cand, k, c0);
     uint32_t pivot, above_all;
-    find_pivot<kChunkThreads, kSelBins>(h.h1, (uint32_t)k_eff, scratch, s_out, &pivot, &above_all);
+    find_pivot<kChunkThreads, kSelBins, kHistCopies>(h.h1, (uint32_t)k_eff, scratch, s_out, &pivot, &above_all,
+                                                     h.h1_stride);
     if (chunk == 0 && threadIdx.x == 0) {
         ctrl[sel * 8 + kCtrlPivot] = pivot;
         ctrl[sel * 8 + kCtrlRank] = (uint32_t)k_eff - above_all;  // rank inside the pivot bin
