@@ -242,6 +242,26 @@ __device__ inline float wave_max(float v) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
 }
 
+// Max and fp64 sum over each 16-lane row (every lane of the row receives its
+// row's result): the first four steps of the wave reductions. Every lane of
+// the row must be active.
+__device__ inline float row16_max(float v) {
+    const float id = -INFINITY;
+    v = fmaxf(v, dpp_or<kDppQuadXor1>(v, id));
+    v = fmaxf(v, dpp_or<kDppQuadXor2>(v, id));
+    v = fmaxf(v, dpp_or<dpp_row_ror(4)>(v, id));
+    v = fmaxf(v, dpp_or<dpp_row_ror(8)>(v, id));
+    return v;
+}
+
+__device__ inline double row16_sum_d(double v) {
+    v += dpp_d0<kDppQuadXor1>(v);
+    v += dpp_d0<kDppQuadXor2>(v);
+    v += dpp_d0<dpp_row_ror(4)>(v);
+    v += dpp_d0<dpp_row_ror(8)>(v);
+    return v;
+}
+
 __device__ inline float wave_sum_f(float v) {
     v += dpp_or<kDppQuadXor1>(v, 0.f);
     v += dpp_or<kDppQuadXor2>(v, 0.f);

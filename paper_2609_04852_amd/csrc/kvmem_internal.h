@@ -43,6 +43,22 @@ constexpr int kMfma16Waves = 2048;
 constexpr int kRowsMaxPerHead = 4096;
 constexpr int kReduceRowsPerPart = 512;
 constexpr int kReduceMaxParts = 64;
+// Small selections merge the per-tile (max, sum exp) pairs of their rows
+// inside the reduction (no separate stats launch) when a relevance value has at
+// most kFusedStatsRows logit rows behind it, each row has at most
+// kFusedStatsParts pairs and all of them together at most kFusedStatsPairs;
+// the vector logits kernel then clears the histograms. (At 32 rows x 16 pairs,
+// 64K tokens, this saves 2 us a step; at 32 x 64 the merge costs more than the
+// launch it replaces.)
+constexpr int kFusedStatsRows = 64;
+constexpr int kFusedStatsParts = 64;
+constexpr int kFusedStatsPairs = 1024;
+// A vector logits launch of at most kLogitsBatchGroups workgroups (one per
+// compute unit) issues all of a tile's loads before its first product: with
+// so few waves each one's chain of load round trips is the kernel's time.
+// With more workgroups the 138 registers this takes cost more occupancy
+// than the batching gains.
+constexpr int kLogitsBatchGroups = 256;
 // Selection: candidates are handled in chunks of kSelChunk (one workgroup
 // each); the key histogram has kSelBins bins (bits 30..19 of the score key),
 // the second level inside the pivot bin kSelBins2 (bits 18..8).
@@ -68,6 +84,8 @@ struct SelectPlan {
     int tiles_per_part;  // index tiles per logit workgroup (0: the persistent 16-row kernel)
     int n_parts;     // logit workgroups along the candidates = partial stats per row
     int n_rsplit;    // row partitions of the block-relevance sum (1: one pass)
+    int fused_stats; // 1: the reduction merges the row stats itself (no stats launch)
+    int batch_loads; // 1: the vector logits kernel issues all of a tile's loads first
     int cand_stride; // row stride of logits and score rows (n_cand rounded up to 64)
     int n_chunks;    // ceil(n_cand / kSelChunk)
     // byte offsets into the workspace
@@ -108,6 +126,10 @@ inline void plan_select_layout(SelectPlan &p) {
         const int nr = p.mode == 0 ? p.n_rows : p.n_q * p.group;  // logit rows behind one relevance value
         int parts = nr / kReduceRowsPerPart;
         p.n_rsplit = parts < 2 ? 1 : (parts > kReduceMaxParts ? kReduceMaxParts : parts);
+        const bool vec = p.rows_per_head <= kScoreVectorRows;
+        p.fused_stats = vec && p.n_rsplit == 1 && nr <= kFusedStatsRows && p.n_parts <= kFusedStatsParts &&
+                        (long long)nr * p.n_parts <= kFusedStatsPairs;
+        p.batch_loads = vec && (long long)p.n_parts * p.n_kv_heads * p.n_layers <= kLogitsBatchGroups;
     }
     p.cand_stride = (p.n_cand + 63) / 64 * 64;
     p.n_chunks = (p.n_cand + kSelChunk - 1) / kSelChunk;

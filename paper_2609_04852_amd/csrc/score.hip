@@ -30,13 +30,19 @@ constexpr int kScoreThreads = 256;
 // 64*tile + i and accumulates its full dot products with the RH query rows of
 // the head.  For every 4-float slice of the head dimension the wave reads 1 KB
 // of contiguous index; the query values are the same for the whole wave.
-template <int D, int RH>
+template <int D, int RH, bool BATCH>
 __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
     const float *__restrict__ q, const float *__restrict__ index, int n_blocks, int n_kv_heads,
     int n_q_heads, int group, int n_q, int n_sink, int n_cand, int64_t cand_stride, int tile_lo,
     int n_tiles, int n_parts, float scale, float *__restrict__ logits, float *__restrict__ tmax,
-    double *__restrict__ tsum) {
+    double *__restrict__ tsum, uint32_t *__restrict__ hist, int hist_words) {
     constexpr int NW = kScoreThreads / kWave;
+    // with the row stats merged in the reduction, the histograms it fills are cleared here
+    if (hist_words > 0) {
+        const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+        const int n_wg = gridDim.x * gridDim.y * gridDim.z;
+        for (int i = wg * kScoreThreads + threadIdx.x; i < hist_words; i += n_wg * kScoreThreads) hist[i] = 0u;
+    }
     __shared__ float sm_m[NW][RH];
     __shared__ double sm_s[NW][RH];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -58,13 +64,29 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_kernel(
         const int64_t tiles_per_layer = index_tiles(n_blocks);
         const float *src = index + (((int64_t)l * tiles_per_layer + tile) * n_kv_heads + g) *
                                        (int64_t)(D / 4) * (kIndexTile * 4) + lane * 4;
+        if constexpr (BATCH) {  // every load of the tile in flight at once
+            float4 xs[D / 4];
 #pragma unroll
-        for (int j4 = 0; j4 < D / 4; ++j4) {  // unrolled: the compiler keeps several loads in flight
-            const float4 x = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
+            for (int j4 = 0; j4 < D / 4; ++j4) xs[j4] = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
+            __builtin_amdgcn_sched_barrier(0);  // the scheduler keeps every load above the products
 #pragma unroll
-            for (int r = 0; r < RH; ++r) {
-                const float4 qv = *reinterpret_cast<const float4 *>(q + qrow[r] * D + j4 * 4);
-                acc[r] += qv.x * x.x + qv.y * x.y + qv.z * x.z + qv.w * x.w;
+            for (int j4 = 0; j4 < D / 4; ++j4) {
+                const float4 x = xs[j4];
+#pragma unroll
+                for (int r = 0; r < RH; ++r) {
+                    const float4 qv = *reinterpret_cast<const float4 *>(q + qrow[r] * D + j4 * 4);
+                    acc[r] += qv.x * x.x + qv.y * x.y + qv.z * x.z + qv.w * x.w;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j4 = 0; j4 < D / 4; ++j4) {  // unrolled: the compiler keeps several loads in flight
+                const float4 x = *reinterpret_cast<const float4 *>(src + j4 * (kIndexTile * 4));
+#pragma unroll
+                for (int r = 0; r < RH; ++r) {
+                    const float4 qv = *reinterpret_cast<const float4 *>(q + qrow[r] * D + j4 * 4);
+                    acc[r] += qv.x * x.x + qv.y * x.y + qv.z * x.z + qv.w * x.w;
+                }
             }
         }
     }
@@ -430,9 +452,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     const double *__restrict__ rinvz, int n_layers, int n_q, int n_q_heads, int n_kv_heads,
     int group, int n_blocks, int n_sink, int n_cand, int64_t cand_stride, int mode,
     float *__restrict__ r32, float *__restrict__ scores, uint32_t *__restrict__ hist,
-    const double *__restrict__ rpart, int n_rsplit) {
+    const double *__restrict__ rpart, int n_rsplit, const float *__restrict__ tmax,
+    const double *__restrict__ tsum, int n_parts, int fused) {
     __shared__ uint32_t lh[kSelBins];
     __shared__ double sm_acc[4][kReduceCols][4];
+    __shared__ float sm_rmax[kFusedStatsRows];
+    __shared__ double sm_rinvz[kFusedStatsRows];
     const int sel = blockIdx.y;
     const int col = threadIdx.x % kReduceCols, rs = threadIdx.x / kReduceCols;
     for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads) lh[i] = 0u;
@@ -440,6 +465,47 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     // mean-all: every (l, m, h) row; group-max: the (m, h in g) rows of layer l
     const int nr = mode == 0 ? n_layers * n_q * n_q_heads : n_q * group;
     const int l = mode == 0 ? 0 : sel / n_kv_heads, g = mode == 0 ? 0 : sel % n_kv_heads;
+    if (fused) {
+        // the rows' max and 1 / Z from their per-tile pairs (the merge of
+        // score_stats, in another order): one 16-lane DPP row per logit row,
+        // rows grp + 16 j, every pair loaded at once (clamped, no branch)
+        constexpr int NG = kScoreThreads / 16;
+        constexpr int RPG = kFusedStatsRows / NG, PPL = kFusedStatsParts / 16;
+        const int grp = threadIdx.x / 16, l16 = threadIdx.x % 16;
+        float tmv[RPG][PPL];
+        double tsv[RPG][PPL];
+#pragma unroll
+        for (int j = 0; j < RPG; ++j) {
+            const int i = min(grp + NG * j, nr - 1);
+            const int64_t row = mode == 0 ? (int64_t)i
+                                          : ((int64_t)l * n_q + i / group) * n_q_heads + g * group + i % group;
+#pragma unroll
+            for (int u = 0; u < PPL; ++u) {
+                const int k = min(l16 + 16 * u, n_parts - 1);
+                tmv[j][u] = tmax[row * n_parts + k];
+                tsv[j][u] = tsum[row * n_parts + k];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < RPG; ++j) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < PPL; ++u) mx = l16 + 16 * u < n_parts ? fmaxf(mx, tmv[j][u]) : mx;
+            mx = row16_max(mx);
+            double z = 0.0;
+#pragma unroll
+            for (int u = 0; u < PPL; ++u)
+                if (l16 + 16 * u < n_parts && tmv[j][u] != -INFINITY)
+                    z += tsv[j][u] * exp((double)tmv[j][u] - (double)mx);
+            z = row16_sum_d(z);
+            const int i = grp + NG * j;
+            if (l16 == 0 && i < nr) {
+                sm_rmax[i] = mx;
+                sm_rinvz[i] = 1.0 / z;
+            }
+        }
+        __syncthreads();
+    }
     double acc[4] = {0.0, 0.0, 0.0, 0.0};
     if (c0 < n_cand && rpart) {
         // the row partitions' partials, in order (slice 0 only)
@@ -456,8 +522,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
             const int64_t row = mode == 0 ? (int64_t)i
                                           : ((int64_t)l * n_q + i / group) * n_q_heads + g * group + i % group;
             const float4 x = *reinterpret_cast<const float4 *>(logits + row * cand_stride + c0);
-            const float mx = rmax[row];
-            const double iz = rinvz[row];
+            const float mx = fused ? sm_rmax[i] : rmax[row];
+            const double iz = fused ? sm_rinvz[i] : rinvz[row];
             const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -507,28 +573,35 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
 
 template <int D, int RH>
 hipError_t launch_logits(const SelectPlan &p, const float *q, const float *index, float scale,
-                         float *logits, float *tmax, double *tsum, hipStream_t stream) {
+                         float *logits, float *tmax, double *tsum, uint32_t *hist, hipStream_t stream) {
     dim3 grid(p.n_parts, p.n_kv_heads, p.n_layers);
-    hipLaunchKernelGGL((score_logits_kernel<D, RH>), grid, dim3(kScoreThreads), 0, stream, q, index,
-                       p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
-                       (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
-                       tsum);
+    const int hist_words = p.fused_stats ? p.n_sel * kSelHistWords : 0;
+    if (p.batch_loads)
+        hipLaunchKernelGGL((score_logits_kernel<D, RH, true>), grid, dim3(kScoreThreads), 0, stream, q, index,
+                           p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
+                           (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
+                           tsum, hist, hist_words);
+    else
+        hipLaunchKernelGGL((score_logits_kernel<D, RH, false>), grid, dim3(kScoreThreads), 0, stream, q, index,
+                           p.n_blocks, p.n_kv_heads, p.n_q_heads, p.group, p.n_q, p.n_sink, p.n_cand,
+                           (int64_t)p.cand_stride, p.tile_lo, p.n_tiles, p.n_parts, scale, logits, tmax,
+                           tsum, hist, hist_words);
     return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_logits_d(const SelectPlan &p, const float *q, const float *index, float scale,
-                           float *logits, float *tmax, double *tsum, hipStream_t stream) {
+                           float *logits, float *tmax, double *tsum, uint32_t *hist, hipStream_t stream) {
     static_assert(kScoreVectorRows == 8, "vector kernels for 1 to 8 rows");
     switch (p.rows_per_head) {
-        case 1: return launch_logits<D, 1>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 2: return launch_logits<D, 2>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 3: return launch_logits<D, 3>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 4: return launch_logits<D, 4>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 5: return launch_logits<D, 5>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 6: return launch_logits<D, 6>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 7: return launch_logits<D, 7>(p, q, index, scale, logits, tmax, tsum, stream);
-        case 8: return launch_logits<D, 8>(p, q, index, scale, logits, tmax, tsum, stream);
+        case 1: return launch_logits<D, 1>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 2: return launch_logits<D, 2>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 3: return launch_logits<D, 3>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 4: return launch_logits<D, 4>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 5: return launch_logits<D, 5>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 6: return launch_logits<D, 6>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 7: return launch_logits<D, 7>(p, q, index, scale, logits, tmax, tsum, hist, stream);
+        case 8: return launch_logits<D, 8>(p, q, index, scale, logits, tmax, tsum, hist, stream);
         case 9: case 10: case 11: case 12: case 13: case 14: case 15: case 16: {
             dim3 grid(p.n_parts / 4, p.n_kv_heads, p.n_layers);
             hipLaunchKernelGGL((score_logits_mfma16_kernel<D>), grid, dim3(kScoreThreads), 0, stream, q, index,
@@ -562,12 +635,14 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
     uint32_t *hist = reinterpret_cast<uint32_t *>(ws + p.off_hist);
     hipError_t e = hipSuccess;
     if (p.n_cand > 0) {  // with no candidate the view is sink + recent only
-        e = p.head_dim == 128 ? launch_logits_d<128>(p, q, index, scale, logits, tmax, tsum, stream)
-                              : launch_logits_d<64>(p, q, index, scale, logits, tmax, tsum, stream);
+        e = p.head_dim == 128 ? launch_logits_d<128>(p, q, index, scale, logits, tmax, tsum, hist, stream)
+                              : launch_logits_d<64>(p, q, index, scale, logits, tmax, tsum, hist, stream);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(score_stats_kernel, dim3(p.n_rows), dim3(kScoreThreads), 0, stream, tmax, tsum,
-                           p.n_parts, rmax, rinvz, hist, p.n_sel * kSelHistWords);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (!p.fused_stats) {
+            hipLaunchKernelGGL(score_stats_kernel, dim3(p.n_rows), dim3(kScoreThreads), 0, stream, tmax, tsum,
+                               p.n_parts, rmax, rinvz, hist, p.n_sel * kSelHistWords);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
     // at least one workgroup per row, which also marks the reserved blocks' scores
     const int n_red = (p.n_cand + kReduceCands - 1) / kReduceCands;
@@ -582,7 +657,7 @@ hipError_t launch_select(const SelectPlan &p, const float *q, const float *index
     hipLaunchKernelGGL(score_reduce_kernel, dim3(n_red > 0 ? n_red : 1, p.n_sel), dim3(kScoreThreads), 0, stream,
                        logits, rmax, rinvz, p.n_layers, p.n_q, p.n_q_heads, p.n_kv_heads, p.group,
                        p.n_blocks, p.n_sink, p.n_cand, (int64_t)p.cand_stride, p.mode, r32, scores, hist, rpart,
-                       p.n_rsplit);
+                       p.n_rsplit, tmax, tsum, p.n_parts, p.fused_stats && p.n_cand > 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk(p, block_to_page, view_blocks, view_pages, ws, stream);
 }

@@ -537,6 +537,48 @@ def test_all_equal_scores_beyond_2_16(k):
     assert vb.tolist() == list(range(k)) + list(range(m - 5, m))
 
 
+# ---- Rows of 63 to 16,385 candidates with ties (up to 17 selection chunks) ----
+@pytest.mark.parametrize("n_cand,k", [(16384, 1), (16384, 9000), (16384, 16384), (16385, 9000), (1000, 999),
+                                      (63, 10)])
+def test_all_equal_scores_small_rows(n_cand, k):
+    """Identical scores, from one partial chunk to 16 full chunks and one more
+    candidate, k from 1 to every candidate: the selection is the k lowest ids,
+    in order, after the sinks and before the recent window."""
+    m = n_cand + 3 + 5
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", m, 3, 5, 1, W.MEAN_ALL, k, planted=0)
+    log(f"[case] all scores equal, {cfg.n_candidates} candidates, k={k}")
+    w = W.generate(cfg, 65, with_values=False)
+    kp = np.broadcast_to(w.k_pool[0][:1], w.k_pool[0].shape).copy()
+    st = LayerState(cfg, kp, None, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    vb = st.view_blocks.cpu().numpy()[0]
+    assert vb.tolist() == list(range(3 + k)) + list(range(m - 5, m))
+    np.testing.assert_array_equal(st.view_pages.cpu().numpy()[0], w.block_to_page[vb])
+
+
+@pytest.mark.parametrize("n_cand,mode", [(16384, W.MEAN_ALL), (12000, W.MAX_GROUP), (16385, W.MEAN_ALL)])
+def test_exact_ties_small_rows(n_cand, mode):
+    """Pages copied from 40 sources: ~400 exact ties per score, and the budget
+    ends inside a tie group, with 4 query rows per KV head."""
+    m, extra = n_cand + 2 + 4, n_cand // 3 + 7
+    cfg = shape_cfg(2, 8, 128, 16, "bf16", m, 2, 4, 1, mode, extra, planted=0)
+    log(f"[case] exact ties, {cfg.n_candidates} candidates, mode {mode}")
+    w = W.generate(cfg, 66, with_values=False)
+    kp = w.k_pool[0]
+    kp[:] = kp[np.random.default_rng(2).integers(0, 40, cfg.n_blocks)]
+    index_ref = oracle.mean_k(kp, w.block_to_page)
+    rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 2, cfg.n_recent, oracle_mode(cfg))
+    k_eff = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, 16, cfg.n_blocks, 2, cfg.n_recent)
+    vb_ref, _ = oracle.select(rel, 2, cfg.n_recent, k_eff, w.block_to_page)
+    st = LayerState(cfg, kp, None, w.block_to_page)
+    st.build_index()
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(st.view_blocks.cpu().numpy(), vb_ref)
+
+
 # ---- Exact ties at the threshold in rows beyond 2^17 candidates ------------
 def test_exact_ties_140k_candidates():
     """140,000 candidates whose pages copy one of 100 source pages: ~1,400
