@@ -169,7 +169,11 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     };
     float4 xa[NC], xb[NC];
     int gi = part;
-    if (gi < n_groups) load(gi, xa);
+    // every load is issued unconditionally at a clamped (in-bounds) group:
+    // behind a branch the compiler must wait at the join for every load,
+    // including the prefetch just issued
+    const int g_last = n_groups - 1;
+    load(min(gi, g_last), xa);
     // B operand: q[row r16][16c + 4kg + e] (the scale is applied to the sum)
     float qv[NC][4];
 #pragma unroll
@@ -222,11 +226,11 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     // current group's products
     while (gi < n_groups) {
         const int g1 = gi + n_parts;
-        if (g1 < n_groups) load(g1, xb);
+        load(min(g1, g_last), xb);
         compute(gi, xa);
         if (g1 >= n_groups) break;
         const int g2 = g1 + n_parts;
-        if (g2 < n_groups) load(g2, xa);
+        load(min(g2, g_last), xa);
         compute(g1, xb);
         gi = g2;
     }
