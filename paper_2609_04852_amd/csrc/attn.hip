@@ -36,6 +36,31 @@ namespace {
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = kAttnWaves * kWave;
 
+// Stages the n_pp (>= 1) page ids of a split into LDS: every thread's loads
+// are issued together (clamped indexes, no branch), so the prologue takes one
+// memory round trip instead of one per id a thread holds.  An id outside
+// [0, n_pages) is stored as page 0 (never read: the caller's partial becomes
+// NaN); returns whether this thread saw one.
+template <int NT>
+__device__ inline bool stage_page_ids(const int32_t *__restrict__ vpages, int p_begin, int n_pp, int64_t n_pages,
+                                      int32_t *sm_pg) {
+    constexpr int PER = (kAttnMaxPages + NT - 1) / NT;
+    int32_t v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) v[u] = vpages[p_begin + min((int)threadIdx.x + NT * u, n_pp - 1)];
+    bool bad = false;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int i = threadIdx.x + NT * u;
+        if (i < n_pp) {
+            const bool ok = v[u] >= 0 && (int64_t)v[u] < n_pages;
+            sm_pg[i] = ok ? v[u] : 0;
+            bad |= !ok;
+        }
+    }
+    return bad;
+}
+
 template <typename T, int D, int BT, int RH>
 __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
     const float *__restrict__ q, const T *__restrict__ k_pool, const T *__restrict__ v_pool,
@@ -229,12 +254,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_row16_kernel(
     // become page 0 and make this split's partial NaN)
     if (threadIdx.x == 0) sm_bad = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < p_end - p_begin; i += kAttnThreads) {
-        const int32_t pg = vpages[p_begin + i];
-        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
-        sm_pg[i] = ok ? pg : 0;
-        if (!ok) sm_bad = 1;
-    }
+    if (stage_page_ids<kAttnThreads>(vpages, p_begin, p_end - p_begin, n_pages, sm_pg)) sm_bad = 1;
     __syncthreads();
 
     float qr[RH][VEC];
@@ -544,12 +564,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_mfma16_kernel(
     // become page 0 and make this split's partial NaN)
     if (threadIdx.x < kAttnWaves) sm_bad[threadIdx.x] = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < p_end - p_begin; i += kAttnThreads) {
-        const int32_t pg = vpages[p_begin + i];
-        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
-        sm_pg[i] = ok ? pg : 0;
-        if (!ok) sm_bad[0] = 1;
-    }
+    if (stage_page_ids<kAttnThreads>(vpages, p_begin, p_end - p_begin, n_pages, sm_pg)) sm_bad[0] = 1;
     __syncthreads();
     const bool any_bad = sm_bad[0] != 0;
 
@@ -802,13 +817,8 @@ __global__ __launch_bounds__(NW * kWave) void attn_mfma_rows_kernel(
     const int p_end = min(n_view, p_begin + pages_per_split);
     const int n_tok = (p_end - p_begin) * BT - (p_end == n_view ? BT - last_page_tokens : 0);
     const int n_tiles = (n_tok + kMfmaTile - 1) / kMfmaTile;
-    bool bad = false;
-    for (int i = threadIdx.x; i < p_end - p_begin; i += NT) {
-        const int32_t pg = vpages[p_begin + i];
-        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
-        sm_pg[i] = ok ? pg : 0;  // an invalid id is never read; the split's partial becomes NaN
-        bad |= !ok;
-    }
+    // an invalid id is never read; the split's partial becomes NaN
+    const bool bad = stage_page_ids<NT>(vpages, p_begin, p_end - p_begin, n_pages, sm_pg);
     const bool any_bad = __syncthreads_or(bad) != 0;
 
     // Q^T operand of this wave's 16 rows, hi + lo bf16 (padding rows are zero)
