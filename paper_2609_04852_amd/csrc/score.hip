@@ -185,14 +185,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_logits_mfma16_kernel(
     float mrun = -INFINITY;  // row r16 (the same in its 4 kg lanes)
     double srun = 0.0;
     auto compute = [&](int gj, const float4 (&x)[NC]) {
-        f64x4_t st = f64x4_t{0.0, 0.0, 0.0, 0.0};
+        // two accumulator chains, so that a wave's products do not each wait
+        // for the one before (20.7 against 21.0 us per MTP layer; four: 20.8)
+        f64x4_t st = f64x4_t{0.0, 0.0, 0.0, 0.0}, st1 = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             const float xv[4] = {x[c].x, x[c].y, x[c].z, x[c].w};
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
+            for (int e = 0; e < 4; e += 2) {
                 st = __builtin_amdgcn_mfma_f64_16x16x4f64((double)xv[e], (double)qv[c][e], st, 0, 0, 0);
+                st1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)xv[e + 1], (double)qv[c][e + 1], st1, 0, 0, 0);
+            }
         }
+        st += st1;
         // logits of blocks kg + 4i of the group, and the online row stats
         const int64_t c0 = (int64_t)(tile_lo + gj / NW) * kIndexTile + 16 * (gj % NW) + kg - n_sink;
         float s[4];
