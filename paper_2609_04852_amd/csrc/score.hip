@@ -576,8 +576,15 @@ __global__ __launch_bounds__(kScoreThreads) void score_reduce_kernel(
     }
     __syncthreads();
     uint32_t *gh = hist + ((int64_t)(blockIdx.x % kHistCopies) * gridDim.y + sel) * kSelBins;
-    for (int i = threadIdx.x; i < kSelBins; i += kScoreThreads)
-        if (lh[i]) atomicAdd(&gh[i], lh[i]);
+    // the thread's bins read from LDS at once, then the non-empty ones added
+    constexpr int PER = kSelBins / kScoreThreads;
+    static_assert(PER * kScoreThreads == kSelBins, "bins split evenly");
+    uint32_t cnt[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) cnt[u] = lh[threadIdx.x + kScoreThreads * u];
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+        if (cnt[u]) atomicAdd(&gh[threadIdx.x + kScoreThreads * u], cnt[u]);
 }
 
 template <int D, int RH>

@@ -164,8 +164,15 @@ __global__ __launch_bounds__(kChunkThreads) void sel_refine_kernel(
             atomicAdd(&lh[bin2(k[e])], 1u);
         }
     __syncthreads();
-    for (int i = threadIdx.x; i < kSelBins2; i += kChunkThreads)
-        if (lh[i]) atomicAdd(&h.h2[i], lh[i]);
+    // the thread's bins read from LDS at once, then the non-empty ones added
+    constexpr int PER = kSelBins2 / kChunkThreads;
+    static_assert(PER * kChunkThreads == kSelBins2, "bins split evenly");
+    uint32_t cnt[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) cnt[u] = lh[threadIdx.x + kChunkThreads * u];
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+        if (cnt[u]) atomicAdd(&h.h2[threadIdx.x + kChunkThreads * u], cnt[u]);
 }
 
 struct FinishShared {
