@@ -520,6 +520,32 @@ def test_4m_history_select():
     log(f"  selection ok: {stats}, worst score rel err {worst:.2e}")
 
 
+def test_max_candidates_select():
+    """The largest selection row the boundary takes: 2^20 candidates (1,024
+    selection chunks; a 16M-token history in 16-token blocks), one KV head
+    with d = 64 so that the K pool stays at 2 GiB. Index bitwise, selection
+    and scores against the oracle."""
+    m = (1 << 20) + 8
+    cfg = shape_cfg(1, 4, 64, 16, "bf16", m, 0, 8, 1, W.MEAN_ALL, 1 << 19, planted=64)
+    assert cfg.n_candidates == 1 << 20
+    log(f"[case] {cfg.n_candidates} candidates (the maximum), k = 2^19")
+    w = W.generate(cfg, 67, with_values=False)
+    index_ref = oracle.mean_k(w.k_pool[0], w.block_to_page)
+    rel = oracle.block_relevance(w.q[0, :1], index_ref[None], 0, cfg.n_recent)
+    k_eff = oracle.k_eff(cfg.budget_tokens, cfg.budget_tokens, 16, cfg.n_blocks, 0, cfg.n_recent)
+    vb_ref, _ = oracle.select(rel, 0, cfg.n_recent, k_eff, w.block_to_page)
+    st = LayerState(cfg, w.k_pool[0], None, w.block_to_page)
+    st.build_index()
+    torch.cuda.synchronize()
+    assert_index_bitwise(st.index_rows(), index_ref)
+    st.select(torch.from_numpy(np.ascontiguousarray(w.q[0, :1])).cuda())
+    torch.cuda.synchronize()
+    stats = check_selection(st.view_blocks.cpu().numpy(), st.view_pages.cpu().numpy(), rel, w.block_to_page, 0,
+                            cfg.n_recent, k_eff, ref_view=vb_ref)
+    worst = check_scores(st.scores.cpu().numpy(), rel, 0, cfg.n_recent)
+    log(f"  selection ok: {stats}, worst score rel err {worst:.2e}")
+
+
 @pytest.mark.parametrize("k", [40000, 69990])
 def test_all_equal_scores_beyond_2_16(k):
     """70,000 candidates with identical scores: the selection is the k lowest ids,
