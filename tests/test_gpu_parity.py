@@ -520,6 +520,14 @@ def test_4m_history_select():
     log(f"  selection ok: {stats}, worst score rel err {worst:.2e}")
 
 
+@pytest.mark.parametrize("mode", [W.MEAN_ALL, W.MAX_GROUP])
+def test_max_rows_per_head(mode):
+    """The most query rows per KV head the boundary takes: 4,096 (G = 8 and
+    512 query tokens), through scoring in 16-row chunks, the row-partitioned
+    relevance sum and the many-row attention, end to end."""
+    run_case(shape_cfg(2, 16, 64, 16, "bf16", 240, 1, 4, 512, mode, 60), 71)
+
+
 def test_max_candidates_select():
     """The largest selection row the boundary takes: 2^20 candidates (1,024
     selection chunks; a 16M-token history in 16-token blocks), one KV head
