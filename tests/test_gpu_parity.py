@@ -171,6 +171,15 @@ def test_budget_extremes(which):
     run_case(cfg, 3, budget=budget)
 
 
+@pytest.mark.parametrize("k", [0, 1])
+@pytest.mark.parametrize("mode", [W.MEAN_ALL, W.MAX_GROUP])
+def test_single_candidate(k, mode):
+    """Three blocks: a sink, one candidate and a recent block. The candidate's
+    relevance is exactly n_q (a softmax over one block); it is kept when the
+    budget leaves room for it and dropped otherwise."""
+    run_case(shape_cfg(2, 8, 64, 16, "bf16", 3, 1, 1, 1, mode, k, planted=0), 73)
+
+
 def test_partial_last_page():
     cfg = shape_cfg(2, 8, 128, 32, "bf16", 400, 0, 3, 2, W.MEAN_ALL, 60)
     run_case(cfg, 5, lpt=7)
