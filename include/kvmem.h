@@ -76,7 +76,7 @@ typedef enum {
     KVMEM_ERR_NULL = -1,        /* a required pointer is NULL */
     KVMEM_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
     KVMEM_ERR_DTYPE = -3,       /* unknown kv_dtype */
-    KVMEM_ERR_UNSUPPORTED = -4, /* valid, but not a shape this build handles */
+    KVMEM_ERR_UNSUPPORTED = -4, /* valid, but not a shape the library handles */
     KVMEM_ERR_BUDGET = -5,      /* active budget cannot hold sink + recent (Eq. 7) */
     KVMEM_ERR_WORKSPACE = -6,   /* workspace missing or smaller than required */
     KVMEM_ERR_ALIGN = -7,       /* a device pointer is not 16-byte aligned */

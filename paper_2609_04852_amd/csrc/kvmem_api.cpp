@@ -162,7 +162,7 @@ kvmem_status make_attn_plan(const kvmem_geom *g, int32_t n_q, int32_t n_sel, int
     p.last_page_tokens = last_page_tokens;
     kvmem::plan_attn_layout(p);
     if (p.n_splits > kvmem::kAttnMaxSplits)
-        return fail(KVMEM_ERR_UNSUPPORTED, "a view of %d pages is longer than this build handles", n_view);
+        return fail(KVMEM_ERR_UNSUPPORTED, "a view of %d pages is longer than the library handles", n_view);
     return KVMEM_OK;
 }
 
